@@ -1,0 +1,558 @@
+// Host side of libhermes.so: argument and state validation, per-layer
+// bookkeeping, and the launches of the gfx950 kernels on the caller's stream.
+// Every check runs before the first launch of a call, so a rejected call
+// leaves device data and host lengths untouched.
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <new>
+#include <utility>
+#include <vector>
+
+#include "hermes_internal.h"
+
+using namespace hermes;
+
+namespace {
+
+constexpr double kLog2e = 1.4426950408889634;
+constexpr size_t kAlign = 256;
+
+size_t round_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+struct Layout {
+  size_t tab, lse, keys, kept, total;
+  int64_t lse_lstride, keys_lstride, kept_lstride;
+};
+
+int max_budget(const hermes_config *c) {
+  int m = 1;
+  for (int l = 0; l < c->n_layers; ++l) m = c->budget[l] > m ? c->budget[l] : m;
+  return m;
+}
+
+int check_config(const hermes_config *c) {
+  if (c == nullptr) return HERMES_EINVAL;
+  if (c->n_layers < 1 || c->n_layers > HERMES_MAX_LAYERS) return HERMES_EINVAL;
+  if (c->n_kv_heads < 1 || c->n_q_heads < c->n_kv_heads) return HERMES_EINVAL;
+  if (c->n_q_heads % c->n_kv_heads != 0) return HERMES_EINVAL;
+  if (c->head_dim != 64 && c->head_dim != 128) return HERMES_ENOTSUP;
+  if (c->max_chunk < 1 || c->max_cap < 1) return HERMES_EINVAL;
+  const int64_t packed = (int64_t)c->max_chunk * (c->n_q_heads / c->n_kv_heads);
+  if (packed > (int64_t)1 << 30) return HERMES_EINVAL;
+  if (c->budget == nullptr) return HERMES_EINVAL;
+  for (int l = 0; l < c->n_layers; ++l) {
+    if (c->budget[l] < 1) return HERMES_EINVAL;
+    if (c->layer_class != nullptr && (c->layer_class[l] < HERMES_SHALLOW ||
+                                      c->layer_class[l] > HERMES_DEEP))
+      return HERMES_EINVAL;
+    if (c->lambda != nullptr &&
+        !(std::isfinite(c->lambda[l]) && c->lambda[l] >= 0.f && c->lambda[l] <= 1.f))
+      return HERMES_EINVAL;
+  }
+  if (c->alpha_mode != 0 && c->alpha_mode != 1) return HERMES_EINVAL;
+  if (c->align_mode != 0 && c->align_mode != 1) return HERMES_EINVAL;
+  if (!std::isfinite(c->omega0) || !std::isfinite(c->gamma)) return HERMES_EINVAL;
+  if (!std::isfinite(c->forget_rate) || !std::isfinite(c->sm_scale)) return HERMES_EINVAL;
+  return HERMES_OK;
+}
+
+Layout layout_of(const hermes_config *c) {
+  Layout s;
+  s.lse_lstride = (int64_t)c->n_q_heads * c->max_chunk;
+  s.keys_lstride = c->max_cap;
+  s.kept_lstride = max_budget(c);
+  size_t off = 0;
+  s.tab = off;
+  off = round_up(off + sizeof(LayerTable) * c->n_layers);
+  s.lse = off;
+  off = round_up(off + sizeof(float) * (size_t)s.lse_lstride * c->n_layers);
+  s.keys = off;
+  off = round_up(off + sizeof(uint32_t) * (size_t)s.keys_lstride * c->n_layers);
+  s.kept = off;
+  off = round_up(off + sizeof(int32_t) * (size_t)s.kept_lstride * c->n_layers);
+  s.total = off;
+  return s;
+}
+
+// 10% shallow, 60% middle, 30% deep (Sec. 4.1), rounded to nearest layer.
+std::vector<int8_t> default_classes(int L) {
+  const int n_sh = (int)std::floor(0.1 * L + 0.5);
+  const int n_dp = (int)std::floor(0.3 * L + 0.5);
+  std::vector<int8_t> c(L, HERMES_MIDDLE);
+  for (int l = 0; l < L; ++l) {
+    if (l < n_sh) c[l] = HERMES_SHALLOW;
+    else if (l >= L - n_dp) c[l] = HERMES_DEEP;
+  }
+  return c;
+}
+
+struct EventPair {
+  hipEvent_t start, stop;
+};
+
+}  // namespace
+
+struct hermes_ctx {
+  int L, Hq, Hkv, D, max_chunk, max_cap;
+  double forget_rate, sm_scale;
+  int alpha_mode, align_mode, force_scores;
+  std::vector<int32_t> budget;
+  std::vector<int8_t> cls;
+  std::vector<double> lambda, omega;
+  std::vector<hermes_layer_buffers> bufs;
+  std::vector<int32_t> len;
+  std::vector<int8_t> cur, appended, buf0_dirty;
+  std::vector<int32_t> init_len;
+  int32_t step_n_new = 0;
+  int n_appended = 0;
+  bool poisoned = false;
+  Layout lay;
+  char *ws = nullptr;
+  LayerTable *d_tab = nullptr;
+  bool prof = false;
+  std::vector<EventPair> used[HERMES_K_COUNT];
+  std::vector<EventPair> pool;
+
+  int prof_begin(int id, hipStream_t s, EventPair *ep) {
+    if (!prof) return HERMES_OK;
+    if (pool.empty()) {
+      EventPair e;
+      if (hipEventCreate(&e.start) != hipSuccess) return HERMES_EHIP;
+      if (hipEventCreate(&e.stop) != hipSuccess) return HERMES_EHIP;
+      pool.push_back(e);
+    }
+    *ep = pool.back();
+    pool.pop_back();
+    if (hipEventRecord(ep->start, s) != hipSuccess) return HERMES_EHIP;
+    (void)id;
+    return HERMES_OK;
+  }
+  int prof_end(int id, hipStream_t s, const EventPair &ep) {
+    if (!prof) return HERMES_OK;
+    if (hipEventRecord(ep.stop, s) != hipSuccess) return HERMES_EHIP;
+    used[id].push_back(ep);
+    return HERMES_OK;
+  }
+  // Launch wrapper: events around the launch when profiling, poison on error.
+  template <typename F>
+  int run(int id, hipStream_t s, F &&launch) {
+    EventPair ep{};
+    if (prof_begin(id, s, &ep) != HERMES_OK) {
+      poisoned = true;
+      return HERMES_EHIP;
+    }
+    if (launch() != hipSuccess) {
+      poisoned = true;
+      return HERMES_EHIP;
+    }
+    if (prof_end(id, s, ep) != HERMES_OK) {
+      poisoned = true;
+      return HERMES_EHIP;
+    }
+    return HERMES_OK;
+  }
+};
+
+extern "C" {
+
+const char *hermes_strerror(int code) {
+  switch (code) {
+    case HERMES_OK: return "ok";
+    case HERMES_EINVAL: return "invalid argument";
+    case HERMES_ECAPACITY: return "buffer capacity exceeded";
+    case HERMES_ESTATE: return "call not allowed in the current state";
+    case HERMES_EHIP: return "HIP runtime error";
+    case HERMES_ENOTSUP: return "unsupported shape";
+    default: return "unknown error";
+  }
+}
+
+size_t hermes_workspace_bytes(const hermes_config *cfg) {
+  if (check_config(cfg) != HERMES_OK) return 0;
+  return layout_of(cfg).total;
+}
+
+int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers, void *workspace,
+                   size_t ws_bytes, hermes_ctx **out) {
+  if (out == nullptr) return HERMES_EINVAL;
+  *out = nullptr;
+  const int rc = check_config(cfg);
+  if (rc != HERMES_OK) return rc;
+  if (layers == nullptr || workspace == nullptr || !aligned(workspace, kAlign)) return HERMES_EINVAL;
+  const Layout lay = layout_of(cfg);
+  if (ws_bytes < lay.total) return HERMES_ECAPACITY;
+  const int L = cfg->n_layers;
+  for (int l = 0; l < L; ++l) {
+    const hermes_layer_buffers &b = layers[l];
+    for (int p = 0; p < 2; ++p) {
+      if (b.k[p] == nullptr || b.v[p] == nullptr || b.pos[p] == nullptr) return HERMES_EINVAL;
+      if (!aligned(b.k[p], 16) || !aligned(b.v[p], 16) || !aligned(b.pos[p], 4))
+        return HERMES_EINVAL;
+    }
+    if (b.w == nullptr || !aligned(b.w, 4)) return HERMES_EINVAL;
+    if (b.cap < 1 || b.init_len < 0) return HERMES_EINVAL;
+    if (b.cap > cfg->max_cap || b.init_len > b.cap || cfg->budget[l] > b.cap)
+      return HERMES_ECAPACITY;
+  }
+
+  hermes_ctx *c = new (std::nothrow) hermes_ctx();
+  if (c == nullptr) return HERMES_EINVAL;
+  c->L = L;
+  c->Hq = cfg->n_q_heads;
+  c->Hkv = cfg->n_kv_heads;
+  c->D = cfg->head_dim;
+  c->max_chunk = cfg->max_chunk;
+  c->max_cap = cfg->max_cap;
+  c->forget_rate = cfg->forget_rate > 0.0 ? cfg->forget_rate : std::ldexp(1.0, -10);
+  c->sm_scale = cfg->sm_scale > 0.0 ? cfg->sm_scale : 1.0 / std::sqrt((double)cfg->head_dim);
+  c->alpha_mode = cfg->alpha_mode;
+  c->align_mode = cfg->align_mode;
+  c->force_scores = cfg->force_scores != 0;
+  c->budget.assign(cfg->budget, cfg->budget + L);
+  c->cls = cfg->layer_class ? std::vector<int8_t>(cfg->layer_class, cfg->layer_class + L)
+                            : default_classes(L);
+  c->lambda.resize(L);
+  static const double kLambda[3] = {0.1, 0.3, 0.4};   // Appendix C
+  for (int l = 0; l < L; ++l)
+    c->lambda[l] = cfg->lambda ? (double)cfg->lambda[l] : kLambda[(int)c->cls[l]];
+  // omega_l for middle layers (Sec. 3.1), l_short/l_long = first/last middle layer.
+  int l_s = -1, l_l = -1;
+  for (int l = 0; l < L; ++l)
+    if (c->cls[l] == HERMES_MIDDLE) {
+      if (l_s < 0) l_s = l;
+      l_l = l;
+    }
+  c->omega.assign(L, 0.0);
+  for (int l = 0; l < L; ++l) {
+    if (c->cls[l] != HERMES_MIDDLE) continue;
+    c->omega[l] = (l_l == l_s) ? cfg->omega0
+                               : cfg->omega0 - cfg->gamma * (double)(l - l_s) / (double)(l_l - l_s);
+  }
+  c->bufs.assign(layers, layers + L);
+  c->len.resize(L);
+  for (int l = 0; l < L; ++l) c->len[l] = layers[l].init_len;
+  c->init_len = c->len;
+  c->cur.assign(L, 0);
+  c->appended.assign(L, 0);
+  c->buf0_dirty.assign(L, 0);
+  c->lay = lay;
+  c->ws = static_cast<char *>(workspace);
+  c->d_tab = reinterpret_cast<LayerTable *>(c->ws + lay.tab);
+
+  std::vector<LayerTable> tab(L);
+  for (int l = 0; l < L; ++l) {
+    LayerTable &t = tab[l];
+    std::memset(&t, 0, sizeof(t));
+    for (int p = 0; p < 2; ++p) {
+      t.k[p] = static_cast<uint16_t *>(layers[l].k[p]);
+      t.v[p] = static_cast<uint16_t *>(layers[l].v[p]);
+      t.pos[p] = layers[l].pos[p];
+    }
+    t.w = layers[l].w;
+    t.s_dbg = layers[l].s_dbg;
+    t.kept_dbg = layers[l].kept_dbg;
+    t.cap = layers[l].cap;
+    t.budget = c->budget[l];
+    t.cls = c->cls[l];
+    t.lambda = c->lambda[l];
+    t.omega = c->omega[l];
+  }
+  if (hipMemcpy(c->d_tab, tab.data(), sizeof(LayerTable) * L, hipMemcpyHostToDevice) !=
+      hipSuccess) {
+    delete c;
+    return HERMES_EHIP;
+  }
+  *out = c;
+  return HERMES_OK;
+}
+
+void hermes_kv_destroy(hermes_ctx *ctx) {
+  if (ctx == nullptr) return;
+  for (auto &v : ctx->used)
+    for (auto &e : v) {
+      (void)hipEventDestroy(e.start);
+      (void)hipEventDestroy(e.stop);
+    }
+  for (auto &e : ctx->pool) {
+    (void)hipEventDestroy(e.start);
+    (void)hipEventDestroy(e.stop);
+  }
+  delete ctx;
+}
+
+int hermes_kv_rewind(hermes_ctx *ctx) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  if (ctx->poisoned) return HERMES_ESTATE;
+  for (int l = 0; l < ctx->L; ++l)
+    if (ctx->buf0_dirty[l]) return HERMES_ESTATE;
+  for (int l = 0; l < ctx->L; ++l) {
+    ctx->len[l] = ctx->init_len[l];
+    ctx->cur[l] = 0;
+    ctx->appended[l] = 0;
+  }
+  ctx->n_appended = 0;
+  ctx->step_n_new = 0;
+  return HERMES_OK;
+}
+
+int hermes_kv_view(const hermes_ctx *ctx, int32_t layer, const void **k, const void **v,
+                   const int32_t **pos, int32_t *len) {
+  if (ctx == nullptr || layer < 0 || layer >= ctx->L) return HERMES_EINVAL;
+  const int p = ctx->cur[layer];
+  if (k) *k = ctx->bufs[layer].k[p];
+  if (v) *v = ctx->bufs[layer].v[p];
+  if (pos) *pos = ctx->bufs[layer].pos[p];
+  if (len) *len = ctx->len[layer];
+  return HERMES_OK;
+}
+
+int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                        const void *v, const int32_t *pos, int32_t n_new, void *out,
+                        void *stream) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  if (ctx->poisoned) return HERMES_ESTATE;
+  const int L = ctx->L;
+  if (layer != HERMES_ALL_LAYERS && (layer < 0 || layer >= L)) return HERMES_EINVAL;
+  if (q == nullptr || k == nullptr || v == nullptr || pos == nullptr || out == nullptr)
+    return HERMES_EINVAL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
+      !aligned(pos, 4))
+    return HERMES_EINVAL;
+  if (n_new < 1 || n_new > ctx->max_chunk) return HERMES_EINVAL;
+  std::vector<int> list;
+  if (layer == HERMES_ALL_LAYERS) {
+    for (int l = 0; l < L; ++l) list.push_back(l);
+  } else {
+    list.push_back(layer);
+  }
+  for (int l : list)
+    if (ctx->appended[l]) return HERMES_ESTATE;
+  if (ctx->n_appended > 0 && n_new != ctx->step_n_new) return HERMES_ESTATE;
+  for (int l : list)
+    if ((int64_t)ctx->len[l] + n_new > ctx->bufs[l].cap) return HERMES_ECAPACITY;
+
+  // Which layers' scores the coming compression needs (Sec. 3.1/3.2): a
+  // non-shallow layer that evicts, or whose shallower neighbour evicts and
+  // smooths with it.
+  auto base_len = [&](int l) { return ctx->appended[l] ? ctx->len[l] - ctx->step_n_new : ctx->len[l]; };
+  auto evicts = [&](int l) { return base_len(l) + n_new > ctx->budget[l]; };
+  auto need_w = [&](int l) {
+    if (ctx->force_scores) return true;
+    if (ctx->cls[l] == HERMES_SHALLOW) return false;
+    return evicts(l) || (l > 0 && evicts(l - 1) && ctx->lambda[l - 1] != 0.0);
+  };
+
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int G = ctx->Hq / ctx->Hkv;
+  const int64_t q_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_new * ctx->Hq * ctx->D : 0;
+  const int64_t kv_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_new * ctx->Hkv * ctx->D : 0;
+  const float scale_log2 = (float)(ctx->sm_scale * kLog2e);
+  (void)G;
+
+  AppendArgs ap;
+  std::memset(&ap, 0, sizeof(ap));
+  ap.tab = ctx->d_tab;
+  ap.kn = static_cast<const uint16_t *>(k);
+  ap.vn = static_cast<const uint16_t *>(v);
+  ap.pos = pos;
+  ap.kv_lstride = kv_ls;
+  ap.row_elems = ctx->Hkv * ctx->D;
+  ap.C = n_new;
+  ap.n_list = (int)list.size();
+
+  AttnArgs at;
+  std::memset(&at, 0, sizeof(at));
+  at.tab = ctx->d_tab;
+  at.q = static_cast<const uint16_t *>(q);
+  at.kn = ap.kn;
+  at.vn = ap.vn;
+  at.out = static_cast<uint16_t *>(out);
+  at.lse = reinterpret_cast<float *>(ctx->ws + ctx->lay.lse);
+  at.q_lstride = q_ls;
+  at.kv_lstride = kv_ls;
+  at.lse_lstride = ctx->lay.lse_lstride;
+  at.Hq = ctx->Hq;
+  at.Hkv = ctx->Hkv;
+  at.C = n_new;
+  at.scale_log2 = scale_log2;
+
+  ColsumArgs cs;
+  std::memset(&cs, 0, sizeof(cs));
+  cs.tab = ctx->d_tab;
+  cs.q = at.q;
+  cs.kn = ap.kn;
+  cs.vn = ap.vn;
+  cs.lse = at.lse;
+  cs.q_lstride = q_ls;
+  cs.kv_lstride = kv_ls;
+  cs.lse_lstride = at.lse_lstride;
+  cs.Hq = ctx->Hq;
+  cs.Hkv = ctx->Hkv;
+  cs.C = n_new;
+  cs.scale_log2 = scale_log2;
+  int n_cs = 0, max_T = 0;
+
+  for (size_t j = 0; j < list.size(); ++j) {
+    const int l = list[j];
+    const int8_t slot = (int8_t)(layer == HERMES_ALL_LAYERS ? l : 0);
+    ap.T0[j] = at.T0[j] = ctx->len[l];
+    ap.layer_id[j] = at.layer_id[j] = (int8_t)l;
+    ap.slot[j] = at.slot[j] = slot;
+    ap.cur[j] = at.cur[j] = ctx->cur[l];
+    if (need_w(l)) {
+      cs.T0[n_cs] = ctx->len[l];
+      cs.layer_id[n_cs] = (int8_t)l;
+      cs.slot[n_cs] = slot;
+      cs.cur[n_cs] = ctx->cur[l];
+      max_T = ctx->len[l] + n_new > max_T ? ctx->len[l] + n_new : max_T;
+      ++n_cs;
+    }
+  }
+
+  int rc = ctx->run(HERMES_K_APPEND, s, [&] { return launch_append(ap, s); });
+  if (rc != HERMES_OK) return rc;
+  rc = ctx->run(HERMES_K_ATTN, s, [&] { return launch_attention(at, (int)list.size(), ctx->D, s); });
+  if (rc != HERMES_OK) return rc;
+  if (n_cs > 0) {
+    rc = ctx->run(HERMES_K_COLSUM, s, [&] { return launch_colsum(cs, n_cs, max_T, ctx->D, s); });
+    if (rc != HERMES_OK) return rc;
+  }
+  for (int l : list) {
+    ctx->len[l] += n_new;
+    ctx->appended[l] = 1;
+  }
+  ctx->n_appended += (int)list.size();
+  ctx->step_n_new = n_new;
+  return HERMES_OK;
+}
+
+int hermes_compress(hermes_ctx *ctx, void *stream) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  if (ctx->poisoned) return HERMES_ESTATE;
+  if (ctx->n_appended == 0) return HERMES_OK;
+  if (ctx->n_appended != ctx->L) return HERMES_ESTATE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+
+  SelectArgs sa;
+  std::memset(&sa, 0, sizeof(sa));
+  sa.tab = ctx->d_tab;
+  sa.keys = reinterpret_cast<uint32_t *>(ctx->ws + ctx->lay.keys);
+  sa.kept = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.kept);
+  sa.keys_lstride = ctx->lay.keys_lstride;
+  sa.kept_lstride = ctx->lay.kept_lstride;
+  sa.forget_rate = ctx->forget_rate;
+  sa.n_layers = ctx->L;
+  sa.C = ctx->step_n_new;
+  sa.alpha_mode = ctx->alpha_mode;
+  sa.align_mode = ctx->align_mode;
+  GatherArgs ga;
+  std::memset(&ga, 0, sizeof(ga));
+  ga.tab = ctx->d_tab;
+  ga.kept = sa.kept;
+  ga.kept_lstride = sa.kept_lstride;
+  ga.row_elems = ctx->Hkv * ctx->D;
+  int n = 0;
+  for (int l = 0; l < ctx->L; ++l) {
+    sa.len[l] = ctx->len[l];
+    sa.cur[l] = ctx->cur[l];
+    if (ctx->len[l] > ctx->budget[l]) {
+      sa.layer_id[n] = (int8_t)l;
+      ga.layer_id[n] = (int8_t)l;
+      ga.cur[n] = ctx->cur[l];
+      ga.row_start[n + 1] = ga.row_start[n] + ctx->budget[l];
+      ++n;
+    }
+  }
+  sa.n_list = ga.n_list = n;
+  if (n > 0) {
+    int rc = ctx->run(HERMES_K_SELECT, s, [&] { return launch_select(sa, s); });
+    if (rc != HERMES_OK) return rc;
+    rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_gather(ga, s); });
+    if (rc != HERMES_OK) return rc;
+  }
+  for (int l = 0; l < ctx->L; ++l) {
+    if (ctx->len[l] > ctx->budget[l]) {
+      if (ctx->cur[l] == 1) ctx->buf0_dirty[l] = 1;
+      ctx->cur[l] ^= 1;
+      ctx->len[l] = ctx->budget[l];
+    }
+    ctx->appended[l] = 0;
+  }
+  ctx->n_appended = 0;
+  return HERMES_OK;
+}
+
+int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                        const void *v, int32_t n_q, void *out, void *stream) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  if (ctx->poisoned) return HERMES_ESTATE;
+  const int L = ctx->L;
+  if (layer != HERMES_ALL_LAYERS && (layer < 0 || layer >= L)) return HERMES_EINVAL;
+  if (q == nullptr || k == nullptr || v == nullptr || out == nullptr) return HERMES_EINVAL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16))
+    return HERMES_EINVAL;
+  if (n_q < 1 || n_q > ctx->max_chunk) return HERMES_EINVAL;
+  if (ctx->n_appended != 0) return HERMES_ESTATE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  AttnArgs at;
+  std::memset(&at, 0, sizeof(at));
+  at.tab = ctx->d_tab;
+  at.q = static_cast<const uint16_t *>(q);
+  at.kn = static_cast<const uint16_t *>(k);
+  at.vn = static_cast<const uint16_t *>(v);
+  at.out = static_cast<uint16_t *>(out);
+  at.lse = nullptr;
+  at.q_lstride = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_q * ctx->Hq * ctx->D : 0;
+  at.kv_lstride = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_q * ctx->Hkv * ctx->D : 0;
+  at.Hq = ctx->Hq;
+  at.Hkv = ctx->Hkv;
+  at.C = n_q;
+  at.scale_log2 = (float)(ctx->sm_scale * kLog2e);
+  int n = 0;
+  for (int l = 0; l < L; ++l) {
+    if (layer != HERMES_ALL_LAYERS && l != layer) continue;
+    at.T0[n] = ctx->len[l];
+    at.layer_id[n] = (int8_t)l;
+    at.slot[n] = (int8_t)(layer == HERMES_ALL_LAYERS ? l : 0);
+    at.cur[n] = ctx->cur[l];
+    ++n;
+  }
+  return ctx->run(HERMES_K_QUERY, s, [&] { return launch_attention(at, n, ctx->D, s); });
+}
+
+int hermes_select_topk(const float *keys, int32_t n, int32_t k, int32_t *out_idx, void *stream) {
+  if (keys == nullptr || out_idx == nullptr || n < 1 || k < 1) return HERMES_EINVAL;
+  if (!aligned(keys, 4) || !aligned(out_idx, 4)) return HERMES_EINVAL;
+  return launch_topk(keys, n, k, out_idx, static_cast<hipStream_t>(stream)) == hipSuccess
+             ? HERMES_OK
+             : HERMES_EHIP;
+}
+
+int hermes_profile_enable(hermes_ctx *ctx, int on) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  ctx->prof = on != 0;
+  return HERMES_OK;
+}
+
+int hermes_profile_read(hermes_ctx *ctx, int kernel_id, double *ms_total, int64_t *count) {
+  if (ctx == nullptr || kernel_id < 0 || kernel_id >= HERMES_K_COUNT) return HERMES_EINVAL;
+  double total = 0.0;
+  int64_t cnt = 0;
+  for (auto &e : ctx->used[kernel_id]) {
+    if (hipEventSynchronize(e.stop) != hipSuccess) return HERMES_EHIP;
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, e.start, e.stop) != hipSuccess) return HERMES_EHIP;
+    total += ms;
+    ++cnt;
+    ctx->pool.push_back(e);
+  }
+  ctx->used[kernel_id].clear();
+  if (ms_total) *ms_total = total;
+  if (count) *count = cnt;
+  return HERMES_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,115 @@
+// Internal declarations shared by the host entry points (hermes_api.cpp) and
+// the gfx950 kernels (*.hip).  Not part of the public ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "hermes.h"
+
+namespace hermes {
+
+constexpr int kMaxLayers = HERMES_MAX_LAYERS;
+
+// Static per-layer description, uploaded once into the workspace.
+struct LayerTable {
+  uint16_t *k[2];
+  uint16_t *v[2];
+  int32_t *pos[2];
+  float *w;
+  float *s_dbg;
+  int32_t *kept_dbg;
+  int32_t cap;
+  int32_t budget;
+  int32_t cls;
+  int32_t pad_;
+  double lambda;
+  double omega;
+};
+
+// Chunk (or query) attention: launch entry j covers layer layer_id[j], reads
+// cached rows [0, T0[j]) of buffer cur[j] and new rows from the stacked inputs
+// at slot j (stride *_lstride elements), writes out (and lse if non-null).
+struct AttnArgs {
+  const LayerTable *tab;
+  const uint16_t *q, *kn, *vn;
+  uint16_t *out;
+  float *lse;               // [n_layers][Hkv][C*G] log2-domain row LSE, or null
+  int64_t q_lstride, kv_lstride, lse_lstride;
+  int32_t Hq, Hkv, C;
+  float scale_log2;         // sm_scale * log2(e)
+  int32_t T0[kMaxLayers];
+  int8_t layer_id[kMaxLayers];
+  int8_t slot[kMaxLayers];      // index of the layer's inputs in the stacked tensors
+  int8_t cur[kMaxLayers];
+};
+
+// Attention-mass sweep: W_i for every candidate of layer layer_id[j].
+struct ColsumArgs {
+  const LayerTable *tab;
+  const uint16_t *q, *kn, *vn;
+  const float *lse;
+  int64_t q_lstride, kv_lstride, lse_lstride;
+  int32_t Hq, Hkv, C;
+  float scale_log2;
+  int32_t T0[kMaxLayers];
+  int8_t layer_id[kMaxLayers];
+  int8_t slot[kMaxLayers];
+  int8_t cur[kMaxLayers];
+};
+
+// Scoring, smoothing and selection; one workgroup per listed layer.  len and
+// cur are indexed by LAYER (the smoothing reads layer l+1).
+struct SelectArgs {
+  const LayerTable *tab;
+  uint32_t *keys;           // [n_layers][max_cap]
+  int32_t *kept;            // [n_layers][max_budget]
+  int64_t keys_lstride, kept_lstride;
+  double forget_rate;
+  int32_t n_layers, C, alpha_mode, align_mode;
+  int32_t n_list;
+  int32_t len[kMaxLayers];
+  int8_t cur[kMaxLayers];
+  int8_t layer_id[kMaxLayers];
+};
+
+// Order-preserving gather of kept rows into the other buffer of each pair.
+struct GatherArgs {
+  const LayerTable *tab;
+  const int32_t *kept;
+  int64_t kept_lstride;
+  int32_t row_elems;        // Hkv * d
+  int32_t n_list;
+  int32_t row_start[kMaxLayers + 1];   // prefix of kept rows over the list
+  int8_t layer_id[kMaxLayers];
+  int8_t cur[kMaxLayers];
+};
+
+// Append copy: new K/V rows and positions into rows [T0, T0 + C) of the
+// current buffer of each listed layer.
+struct AppendArgs {
+  const LayerTable *tab;
+  const uint16_t *kn, *vn;
+  const int32_t *pos;
+  int64_t kv_lstride;
+  int32_t row_elems, C, n_list;
+  int32_t T0[kMaxLayers];
+  int8_t layer_id[kMaxLayers];
+  int8_t slot[kMaxLayers];
+  int8_t cur[kMaxLayers];
+};
+
+// Launchers (return the hipError_t of the launch).
+hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);
+hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_dim,
+                         hipStream_t s);
+hipError_t launch_select(const SelectArgs &a, hipStream_t s);
+hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
+hipError_t launch_append(const AppendArgs &a, hipStream_t s);
+hipError_t launch_topk(const float *keys, int n, int k, int32_t *out, hipStream_t s);
+
+// Geometry shared by host sizing and kernels.
+constexpr int kAttnRowsPerBlock = 128;   // packed (row, head) pairs per workgroup
+constexpr int kColsumKeysPerBlock = 128; // candidates per workgroup of the sweep
+
+}  // namespace hermes

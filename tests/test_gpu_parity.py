@@ -1,0 +1,131 @@
+"""GPU parity of the HIP path against the fp64 oracle, through the C ABI.
+
+Sizes span several tiles of every kernel plus ragged tails (packed query rows
+not a multiple of 128, candidates not a multiple of 64/128, chunk lengths of
+1 and of several hundred) and the edge cases: empty cache, single-token
+chunk, a budget at least the candidate count (nothing evicted), every layer
+class, G = 1 (no grouping) and G = 7.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import hermes_oracle as orc
+from paper_2601_14724_amd import workloads as wk
+
+from _parity import (check_layer, gen, oracle_caches, oracle_chunks, oracle_config, raw_bits,
+                     run_gpu_step, say)
+
+pytestmark = pytest.mark.gpu
+
+
+def _step_parity(wl, classes=None, lambdas=None, check_w=True, **kw):
+    say(f"[parity] {wl.name}: L={wl.n_layers} Hq={wl.n_q_heads} Hkv={wl.n_kv_heads} "
+        f"d={wl.head_dim} T0={wl.init_len} C={wl.chunk} budgets={wl.budgets[:4]}...")
+    caches, chunks = gen(wl)
+    kv, out, w = run_gpu_step(wl, caches, chunks, layer_class=classes, lambdas=lambdas,
+                              force_scores=True, **kw)
+    ref = orc.stream_step(oracle_caches(caches), oracle_chunks(chunks),
+                          oracle_config(wl, classes=classes, lambdas=lambdas,
+                                        alpha_mode=kw.get("alpha_mode", 0),
+                                        align_mode=kw.get("align_mode", 0)))
+    bits = raw_bits(caches, chunks)
+    worst = {}
+    for l in range(wl.n_layers):
+        st = check_layer(l, kv, out, w, ref, wl.budgets[l], wl.chunk, check_w=check_w,
+                         report=bits)
+        for k, v in st.items():
+            worst[k] = max(worst.get(k, 0), v)
+    say(f"[parity] {wl.name} worst: {worst}")
+    kv.close()
+    return worst
+
+
+ATTN_SHAPES = [
+    # name, Hq, Hkv, d, T0, C, budget
+    ("g7_d64", 14, 2, 64, 100, 50, 400),
+    ("g7_d128", 28, 4, 128, 300, 77, 1000),
+    ("g1_empty_cache", 4, 4, 64, 0, 33, 100),
+    ("g7_one_cached", 7, 1, 128, 1, 129, 400),
+    ("one_token_chunk", 8, 2, 64, 257, 1, 1000),
+    ("g2_ragged", 6, 3, 128, 191, 65, 1000),
+]
+
+
+@pytest.mark.parametrize("name,Hq,Hkv,d,T0,C,budget", ATTN_SHAPES)
+def test_attention_and_mass_parity_no_eviction(name, Hq, Hkv, d, T0, C, budget):
+    wl = wk.custom(f"attn_{name}", 100 + len(name), 2, Hq, Hkv, d, T0, C, (budget, budget))
+    _step_parity(wl, classes=[orc.DEEP, orc.DEEP])
+
+
+@pytest.mark.parametrize("cls", [orc.SHALLOW, orc.MIDDLE, orc.DEEP])
+def test_c1_single_layer_each_class(cls):
+    """1 layer, 0.5B shape, 1024 cached + 196 new, budget 512."""
+    wl = wk.WORKLOADS["c1_0p5b_1layer"]
+    worst = _step_parity(wl, classes=[cls], lambdas=[0.0])
+    assert worst["kept_diff"] <= 2
+
+
+def test_small_multilayer_eviction_all_classes():
+    wl = wk.custom("multi", 120, 10, 14, 2, 64, 300, 97, [150, 170, 200, 230, 260, 290, 320,
+                                                         350, 380, 396])
+    _step_parity(wl)
+
+
+@pytest.mark.parametrize("alpha_mode,align_mode", [(1, 0), (0, 1)])
+def test_alternate_readings(alpha_mode, align_mode):
+    wl = wk.custom("readings", 121, 6, 8, 2, 128, 200, 64, [100, 120, 140, 160, 180, 200])
+    _step_parity(wl, alpha_mode=alpha_mode, align_mode=align_mode)
+
+
+def test_c2_full():
+    """24 layers, 0.5B shape, 4096 cached + 784 new, budget 2048 per layer."""
+    _step_parity(wk.WORKLOADS["c2_0p5b_24layer"])
+
+
+def test_topk_kernel_matches_oracle_with_ties():
+    from paper_2601_14724_amd import hermes as H
+    rng = np.random.default_rng(5)
+    for n, k in [(1, 1), (7, 3), (1000, 999), (5000, 1234), (36000, 16000), (100, 200),
+                 (4096, 4096)]:
+        keys = rng.random(n).astype(np.float32)
+        keys[rng.integers(0, n, n // 5)] = keys[0]           # a block of exact ties
+        say(f"[topk] n={n} k={k}")
+        got = H.select_topk(torch.from_numpy(keys).cuda(), k).cpu().numpy()
+        want = orc.topk_indices(keys.astype(np.float64), k)
+        assert np.array_equal(got, want), (n, k)
+
+
+def test_query_after_compress_matches_oracle():
+    wl = wk.custom("query", 122, 3, 28, 4, 128, 400, 100, (256, 300, 600), query_len=64)
+    say("[query] compress then 64-token query")
+    caches, chunks = gen(wl)
+    kv, out, w = run_gpu_step(wl, caches, chunks)
+    ref = orc.stream_step(oracle_caches(caches), oracle_chunks(chunks), oracle_config(wl))
+    from paper_2601_14724_amd import streaming
+    qry = [wk.gen_query(wl, l) for l in range(wl.n_layers)]
+    qt = {k: streaming.bf16_tensor(np.stack([x[k] for x in qry]), "cuda") for k in ("q", "k", "v")}
+    o = kv.query(qt["q"], qt["k"], qt["v"]).float().cpu().numpy()
+    f64 = wk.bf16_bits_to_f64
+    for l in range(wl.n_layers):
+        # continue the oracle from the GPU's kept set (identical bf16 rows)
+        k_g, v_g, p_g = kv.view(l)
+        cache = orc.LayerCache(k_g.float().double().cpu().numpy(), v_g.float().double().cpu().numpy(),
+                               p_g.cpu().numpy())
+        want = orc.query_attention(cache, f64(qry[l]["q"]), f64(qry[l]["k"]), f64(qry[l]["v"]))
+        err = np.abs(o[l] - want).max()
+        assert err <= 2e-2, (l, err)
+    kv.close()
+
+
+def test_determinism_bitwise():
+    wl = wk.WORKLOADS["c1_0p5b_1layer"]
+    caches, chunks = gen(wl)
+    res = []
+    for _ in range(2):
+        kv, out, w = run_gpu_step(wl, caches, chunks, force_scores=True)
+        res.append((out, w[0], kv.s_dbg[0].cpu().numpy(), kv.kept_dbg[0].cpu().numpy(),
+                    kv.view(0)[0].view(torch.int16).cpu().numpy()))
+        kv.close()
+    for a, b in zip(*res):
+        assert np.array_equal(a, b)

@@ -1,0 +1,92 @@
+"""State machine of the C ABI on a real device: every rejected call returns
+its code before any launch and leaves lengths untouched."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2601_14724_amd import hermes as H
+from paper_2601_14724_amd import streaming, workloads as wk
+
+pytestmark = pytest.mark.gpu
+
+
+def _setup():
+    wl = wk.custom("state", 130, 3, 4, 2, 64, 20, 8, (16, 24, 40))
+    kv = streaming.make_cache(wl, max_chunk=8, cap=40)
+    t = streaming.chunk_tensors(wk.stack_chunks(wl, 0))
+    return wl, kv, t
+
+
+def test_append_compress_state_machine():
+    wl, kv, t = _setup()
+    one = {k: t[k][0].contiguous() for k in ("q", "k", "v")}
+    kv.append(one["q"], one["k"], one["v"], t["pos"], layer=0)
+    with pytest.raises(H.HermesError) as e:
+        kv.append(one["q"], one["k"], one["v"], t["pos"], layer=0)       # twice in one step
+    assert e.value.code == H.ESTATE
+    with pytest.raises(H.HermesError) as e:
+        kv.compress()                                                      # not all layers yet
+    assert e.value.code == H.ESTATE
+    with pytest.raises(H.HermesError) as e:
+        kv.query(one["q"], one["k"], one["v"], layer=1)                    # mid-step query
+    assert e.value.code == H.ESTATE
+    short = {k: one[k][:4].contiguous() for k in one}
+    with pytest.raises(H.HermesError) as e:                                # different n_new
+        kv.append(short["q"], short["k"], short["v"], t["pos"][:4].contiguous(), layer=1)
+    assert e.value.code == H.ESTATE
+    assert kv.length(1) == 20
+    for l in (1, 2):
+        kv.append(one["q"], one["k"], one["v"], t["pos"], layer=l)
+    kv.compress()
+    torch.cuda.synchronize()
+    assert [kv.length(l) for l in range(3)] == [16, 24, 28]
+    kv.compress()                                                          # no-op
+    kv.rewind()
+    assert [kv.length(l) for l in range(3)] == [20, 20, 20]
+    kv.close()
+
+
+def test_capacity_and_argument_errors():
+    wl, kv, t = _setup()
+    ctx = kv.ctx
+    one = {k: t[k][0].contiguous() for k in ("q", "k", "v")}
+    assert H.lib.hermes_append_chunk(ctx, 5, one["q"].data_ptr(), one["k"].data_ptr(),
+                                     one["v"].data_ptr(), t["pos"].data_ptr(), 8,
+                                     one["q"].data_ptr(), None) == H.EINVAL  # layer out of range
+    assert H.lib.hermes_append_chunk(ctx, 0, one["q"].data_ptr() + 2, one["k"].data_ptr(),
+                                     one["v"].data_ptr(), t["pos"].data_ptr(), 8,
+                                     one["q"].data_ptr(), None) == H.EINVAL  # misaligned input
+    assert H.lib.hermes_append_chunk(ctx, H.ALL_LAYERS, t["q"].data_ptr(), t["k"].data_ptr(),
+                                     t["v"].data_ptr(), t["pos"].data_ptr(), 9,
+                                     t["q"].data_ptr(), None) == H.EINVAL   # > max_chunk
+    assert H.lib.hermes_append_chunk(ctx, H.ALL_LAYERS, t["q"].data_ptr(), t["k"].data_ptr(),
+                                     t["v"].data_ptr(), t["pos"].data_ptr(), 0,
+                                     t["q"].data_ptr(), None) == H.EINVAL   # empty chunk
+    # fill layer 2 (budget 40 = cap) up to capacity: 20 + 8 + 8 = 36, next append overflows
+    for _ in range(2):
+        kv.append(t["q"], t["k"], t["v"], t["pos"])
+        kv.compress()
+    torch.cuda.synchronize()
+    assert kv.length(2) == 36
+    with pytest.raises(H.HermesError) as e:
+        kv.append(t["q"], t["k"], t["v"], t["pos"])
+    assert e.value.code == H.ECAPACITY
+    assert [kv.length(l) for l in range(3)] == [16, 24, 36]
+    with pytest.raises(H.HermesError) as e:
+        kv.rewind()                            # layers 0/1 compacted twice: buffer 0 overwritten
+    assert e.value.code == H.ESTATE
+    kv.close()
+
+
+def test_profiling_counts_launches():
+    wl, kv, t = _setup()
+    kv.profile(True)
+    kv.append(t["q"], t["k"], t["v"], t["pos"])
+    kv.compress()
+    ms, n = kv.profile_read(H.K_ATTN)
+    assert n == 1 and ms > 0
+    ms, n = kv.profile_read(H.K_GATHER)
+    assert n == 1
+    ms, n = kv.profile_read(H.K_ATTN)
+    assert n == 0 and ms == 0
+    kv.close()
