@@ -1,0 +1,193 @@
+"""Benchmark of the HERMES streaming step on one MI355X.
+
+A step is one chunk append over every layer (attention, attention mass) plus
+the compression (scoring, smoothing, top-k, gather-compaction) of the 28-layer
+7B-shaped cache: 8192 cached tokens + 784 new (4 frames x 196 tokens) per
+layer, per-layer budgets ramping 2048 -> 6144.  Between steps the context is
+rewound on the host to the untouched initial cache (compaction writes the
+other buffer of each pair), so every timed step does identical work with no
+restore copy.
+
+Prints ONE JSON line:  metric, value (video tokens appended+compressed per
+second), ms_per_step, the roofline of the dominant kernel (HIP events around
+its launches in the timed region), and the fp64 CPU oracle timed on a bounded
+sample of the same workload on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import concurrent.futures as cf
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "video tokens/s appended+compressed (all layers) at 7B shape; % MFMA / HBM peak"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def attention_flops(wl) -> float:
+    """Algorithmic FLOPs of the causal chunk attention over all layers:
+    4 d per visible (query row, candidate, head) triple (QK^T and PV)."""
+    C, T0 = wl.chunk, wl.init_len
+    pairs = wl.n_layers * wl.n_q_heads * (C * T0 + C * (C + 1) // 2)
+    return 4.0 * wl.head_dim * pairs
+
+
+def gather_bytes(wl) -> float:
+    """Algorithmic bytes of the gather: each kept row of K and V read and
+    written once, plus its position (read + write)."""
+    row = wl.n_kv_heads * wl.head_dim * 2
+    T = wl.init_len + wl.chunk
+    kept = sum(min(T, b) for b in wl.budgets if T > b)
+    return kept * (4.0 * row + 8.0)
+
+
+def cpu_baseline(wl, n_layers: int) -> dict:
+    from threadpoolctl import threadpool_info
+
+    from oracle import hermes_oracle as orc
+    from paper_2601_14724_amd import workloads as wk
+    f64 = wk.bf16_bits_to_f64
+    layers = list(range(n_layers))
+    caches = [wk.gen_cache(wl, l) for l in layers]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in layers]
+    oc = [orc.LayerCache(f64(c["k"]), f64(c["v"]), c["pos"].astype(np.int64)) for c in caches]
+    och = [{"q": f64(c["q"]), "k": f64(c["k"]), "v": f64(c["v"]), "pos": c["pos"]} for c in chunks]
+    classes = orc.layer_partition(wl.n_layers)[:n_layers]
+    cfg = orc.OracleConfig(budgets=list(wl.budgets[:n_layers]), classes=classes,
+                           lambdas=orc.smoothing_lambdas(orc.layer_partition(wl.n_layers))[:n_layers])
+    t0 = time.perf_counter()
+    orc.stream_step(oc, och, cfg)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    per_step = dt * wl.n_layers / n_layers
+    return {"value": wl.chunk / per_step, "unit": "video tokens/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"fp64 oracle step (attention+mass, scoring, smoothing, top-k, gather) on "
+                      f"layers 0..{n_layers - 1} of the 28-layer workload, {dt:.1f} s, scaled "
+                      f"x{wl.n_layers}/{n_layers} to the whole step"}
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="c3_7b_28layer")
+    ap.add_argument("--cpu-sample-layers", type=int, default=4)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--calib-copy-mib", type=int, default=0,
+                    help="also run one plain device copy of this many MiB (counter calibration)")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        log("this build runs on one GPU only; --gpus must be 1")
+        return 2
+
+    import torch
+
+    from paper_2601_14724_amd import hermes as H
+    from paper_2601_14724_amd import streaming, workloads as wk
+
+    wl = wk.WORKLOADS[args.workload]
+    log(f"[bench] generating inputs for {wl.name}")
+    with cf.ThreadPoolExecutor(max_workers=8) as ex:
+        caches = list(ex.map(lambda l: wk.gen_cache(wl, l), range(wl.n_layers)))
+        chunks = list(ex.map(lambda l: wk.gen_chunk(wl, 0, l), range(wl.n_layers)))
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    kv = streaming.make_cache(wl, device=dev, caches=caches)
+    st = {k: np.stack([c[k] for c in chunks]) for k in ("q", "k", "v")} | {"pos": chunks[0]["pos"]}
+    t = streaming.chunk_tensors(st, dev)
+    out = torch.empty_like(t["q"])
+    del caches, chunks, st
+
+    def step():
+        kv.rewind()
+        kv.append(t["q"], t["k"], t["v"], t["pos"], out=out)
+        kv.compress()
+
+    log(f"[bench] warmup {args.warmup}")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    kv.profile(True)
+    for kid in range(6):
+        kv.profile_read(kid)
+    log(f"[bench] timing {args.steps} steps")
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kernels = {}
+    for kid, name in enumerate(H.KERNEL_NAMES):
+        ms, cnt = kv.profile_read(kid)
+        if cnt:
+            kernels[name] = {"avg_ms": ms / cnt, "launches": cnt}
+    kv.profile(False)
+
+    if args.calib_copy_mib:
+        n = args.calib_copy_mib * (1 << 20) // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"[bench] calibration copy of {args.calib_copy_mib} MiB done")
+
+    ms_step = 1e3 * elapsed / args.steps
+    value = wl.chunk * args.steps / elapsed
+    fl = attention_flops(wl)
+    att_ms = kernels["attention"]["avg_ms"]
+    achieved = fl / (att_ms * 1e-3) / 1e12
+    roofline = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "kernel": "attn_fwd", "flops_per_launch": fl}
+    gb = gather_bytes(wl)
+    extra = {"kernels_ms": {k: round(v["avg_ms"], 4) for k, v in kernels.items()}}
+    if "gather" in kernels:
+        g = gb / (kernels["gather"]["avg_ms"] * 1e-3) / 1e9
+        extra["gather_GBps"] = round(g, 1)
+        extra["gather_hbm_frac"] = round(g / PEAK_HBM_GBS, 4)
+    if "colsum" in kernels:
+        sweep = attention_flops(wl) / 2 * _mass_layer_fraction(wl)
+        extra["colsum_TFLOPs_executed"] = round(sweep / (kernels["colsum"]["avg_ms"] * 1e-3) / 1e12, 2)
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"[bench] oracle CPU baseline on {args.cpu_sample_layers} layers")
+        cpu = cpu_baseline(wl, args.cpu_sample_layers)
+    rec = {"metric": METRIC, "value": round(value, 1), "unit": "video tokens/s", "n_gpus": 1,
+           "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_step, 4),
+           "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "bf16",
+           "data": "synthetic (seeded Gaussian Q/K/V, low-rank keys, RoPE theta 1e6)",
+           "config": {"workload": wl.name, "n_layers": wl.n_layers, "n_q_heads": wl.n_q_heads,
+                      "n_kv_heads": wl.n_kv_heads, "head_dim": wl.head_dim,
+                      "cached_tokens": wl.init_len, "chunk_tokens": wl.chunk,
+                      "budgets": f"{wl.budgets[0]}..{wl.budgets[-1]} (linear ramp)",
+                      "parallelism": "single GPU"},
+           "roofline": roofline, "cpu_baseline": cpu, **extra}
+    print(json.dumps(rec), flush=True)
+    kv.close()
+    return 0
+
+
+def _mass_layer_fraction(wl) -> float:
+    """Fraction of layers whose attention mass the step computes (the
+    non-shallow ones under the 10/60/30 partition)."""
+    n_sh = int(np.floor(0.1 * wl.n_layers + 0.5))
+    return (wl.n_layers - n_sh) / wl.n_layers
+
+
+if __name__ == "__main__":
+    sys.exit(main())
