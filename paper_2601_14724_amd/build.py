@@ -24,7 +24,10 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", f"-I{INCLUDE}",
 # Packed-FP32 VALU forms stay off: the compiler would otherwise emit them
 # from plain float code.  The host pass warns that it does not know the
 # feature; that warning is harmless.
-DEVICE_ONLY = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops"]
+DEVICE_ONLY = ["-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+               # MFMA results stay in ordinary VGPRs (no accumulator-register copies
+               # before the softmax / attention-mass arithmetic reads them)
+               "-mllvm", "-amdgpu-mfma-vgpr-form"]
 
 
 def _compile(src: str) -> str:

@@ -14,6 +14,8 @@
 // MFMA layout (v_mfma_f32_32x32x16_bf16): lane l supplies A[m = l%32][k = 8(l/32)
 // .. +7] and B[k = 8(l/32) .. +7][n = l%32]; result register j of lane l holds
 // D[m = 8(j/4) + 4(l/32) + j%4][n = l%32].
+#include <type_traits>
+
 #include "hermes_internal.h"
 
 namespace hermes {
@@ -21,13 +23,14 @@ namespace {
 
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short s4 __attribute__((ext_vector_type(4)));
 
 constexpr int BM = kAttnRowsPerBlock;    // packed rows per workgroup (4 waves x 32)
 constexpr int BN = 64;                   // keys per tile
-constexpr int BK = kColsumKeysPerBlock;  // candidates per sweep workgroup (4 waves x 32)
+constexpr int BK = kColsumKeysPerBlock;  // candidates per sweep workgroup (4 waves x 64)
 constexpr int BQ = 64;                   // packed rows per sweep tile
 constexpr int KPAD = 8;                  // u16 padding of K / Q rows in LDS
-constexpr int VPAD = 4;                  // u16 padding of transposed V rows in LDS
+constexpr int VPAD = 16;                 // u16 padding of V rows in LDS
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -39,8 +42,23 @@ __device__ __forceinline__ uint16_t f2bf(float x) {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// 16-byte load through the global (not flat) address space, so outstanding
+// prefetches are tracked by vmcnt only and never delay LDS waits.
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+__device__ __forceinline__ uint4 gload16(const uint16_t *p) {
+  typedef const __attribute__((address_space(1))) u32x4 *gptr;
+  const u32x4 v = *(gptr)(p);
+  return uint4{v.x, v.y, v.z, v.w};
+}
+
+// ds_read_b64_tr_b16: inside each group of 16 lanes, lane j receives element
+// j%4 of the 8-byte rows addressed by lanes j/4, 4 + j/4, 8 + j/4, 12 + j/4.
+__device__ __forceinline__ s4 lds_tr16(const uint16_t *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)p);
+}
+
 template <int D>
-__global__ __launch_bounds__(256) void attn_fwd(AttnArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a) {
   const int j = blockIdx.z;
   const int kv = blockIdx.y;
   const int layer = a.layer_id[j];
@@ -70,24 +88,74 @@ __global__ __launch_bounds__(256) void attn_fwd(AttnArgs a) {
   const bool row_ok = prow < P;
   const int r = row_ok ? prow / G : 0;
   const int h = kv * G + (row_ok ? prow - r * G : 0);
-  const int vis = row_ok ? T0 + r : -1;   // last candidate this row sees
+  const int vis = row_ok ? T0 + r : -1;     // last candidate this row sees
+  const int vis_min = T0 + p0 / G;          // every row of the block sees keys <= vis_min
 
   bf16x8 qf[D / 16];
 #pragma unroll
   for (int kk = 0; kk < D / 16; ++kk) {
-    if (row_ok) {
-      qf[kk] = *reinterpret_cast<const bf16x8 *>(q + ((int64_t)r * Hq + h) * D + 16 * kk + 8 * half);
-    } else {
-      qf[kk] = bf16x8{};
-    }
+    qf[kk] = row_ok ? *reinterpret_cast<const bf16x8 *>(q + ((int64_t)r * Hq + h) * D + 16 * kk + 8 * half)
+                    : bf16x8{};
   }
 
   const int pmax = min(p0 + BM, P) - 1;
   const int nkeys = T0 + pmax / G + 1;
   const int ntiles = (nkeys + BN - 1) / BN;
 
-  __shared__ __attribute__((aligned(16))) uint16_t Ks[BN][D + KPAD];
-  __shared__ __attribute__((aligned(16))) uint16_t Vt[D][BN + VPAD];
+  // Double-buffered K and V tiles, both row-major [key][d]; V is read
+  // transposed by ds_read_b64_tr_b16.  Row pads keep the K reads (16 B per
+  // lane) and the transposed V reads (4 rows x 32 B per 16 lanes) spread
+  // over the LDS banks.
+  __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN][D + KPAD];
+  __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN][D + VPAD];
+
+  constexpr int CH = D / 8;                 // 16-byte chunks per key row and head
+  constexpr int NLD = BN * CH / 256;        // chunks per thread per tensor
+  const int64_t row_stride = (int64_t)Hkv * D;
+  uint4 kreg[NLD], vreg[NLD];
+  // Tiles [0, n_pure) lie wholly in the cache and below every row's causal
+  // limit: they load with plain pointer strides and need no mask.
+  const int n_pure = min(ntiles, T0 / BN);
+  const uint16_t *kpure[NLD], *vpure[NLD];
+#pragma unroll
+  for (int u = 0; u < NLD; ++u) {
+    const int e = tid + u * 256;
+    const int64_t off = (int64_t)(e / CH) * row_stride + kv * D + (e % CH) * 8;
+    kpure[u] = kc + off;
+    vpure[u] = vc + off;
+  }
+  auto load_pure = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      kreg[u] = gload16(kpure[u] + (int64_t)k0 * row_stride);
+      vreg[u] = gload16(vpure[u] + (int64_t)k0 * row_stride);
+    }
+  };
+  auto load_any = [&](int k0) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int e = tid + u * 256;
+      const int kr = e / CH, ch = e % CH;
+      const int i = k0 + kr;
+      uint4 k4 = {0u, 0u, 0u, 0u}, v4 = {0u, 0u, 0u, 0u};
+      if (i < T) {
+        const int64_t off = (i < T0 ? (int64_t)i : (int64_t)(i - T0)) * row_stride + kv * D + ch * 8;
+        k4 = gload16((i < T0 ? kc : kn) + off);
+        v4 = gload16((i < T0 ? vc : vn) + off);
+      }
+      kreg[u] = k4;
+      vreg[u] = v4;
+    }
+  };
+  auto store_tile = [&](int b) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int e = tid + u * 256;
+      const int kr = e / CH, ch = e % CH;
+      *reinterpret_cast<uint4 *>(&Ks[b][kr][ch * 8]) = kreg[u];
+      *reinterpret_cast<uint4 *>(&Vs[b][kr][ch * 8]) = vreg[u];
+    }
+  };
 
   f32x16 o[D / 32];
 #pragma unroll
@@ -95,36 +163,14 @@ __global__ __launch_bounds__(256) void attn_fwd(AttnArgs a) {
   float m_run = -1e30f, l_run = 0.f;
   const float c = a.scale_log2;
 
-  for (int t = 0; t < ntiles; ++t) {
-    const int k0 = t * BN;
-    __syncthreads();
-    constexpr int CH = D / 8;
-    for (int e = tid; e < BN * CH; e += 256) {
-      const int kr = e / CH, ch = e - (e / CH) * CH;
-      const int i = k0 + kr;
-      uint4 k4 = {0u, 0u, 0u, 0u}, v4 = {0u, 0u, 0u, 0u};
-      if (i < T) {
-        const uint16_t *ks, *vs;
-        if (i < T0) {
-          ks = kc + ((int64_t)i * Hkv + kv) * D;
-          vs = vc + ((int64_t)i * Hkv + kv) * D;
-        } else {
-          ks = kn + ((int64_t)(i - T0) * Hkv + kv) * D;
-          vs = vn + ((int64_t)(i - T0) * Hkv + kv) * D;
-        }
-        k4 = *reinterpret_cast<const uint4 *>(ks + ch * 8);
-        v4 = *reinterpret_cast<const uint4 *>(vs + ch * 8);
-      }
-      *reinterpret_cast<uint4 *>(&Ks[kr][ch * 8]) = k4;
-      const uint32_t vw[4] = {v4.x, v4.y, v4.z, v4.w};
-#pragma unroll
-      for (int e2 = 0; e2 < 4; ++e2) {
-        Vt[ch * 8 + 2 * e2][kr] = (uint16_t)(vw[e2] & 0xFFFFu);
-        Vt[ch * 8 + 2 * e2 + 1][kr] = (uint16_t)(vw[e2] >> 16);
-      }
-    }
-    __syncthreads();
+  // transposed-read coordinates of this lane inside its 16-lane group
+  const int g16 = lane >> 4, s16 = lane & 15;
+  const int tr_row = 4 * (g16 >> 1) + (s16 >> 2);
+  const int tr_col = 16 * (g16 & 1) + 4 * (s16 & 3);
 
+  auto compute = [&](int t, auto masked) {
+    const int b = t & 1;
+    const int k0 = t * BN;
     // S^T = K Q^T for two 32-key sub-tiles: lane = query row, register = key.
     f32x16 s[2];
 #pragma unroll
@@ -132,28 +178,38 @@ __global__ __launch_bounds__(256) void attn_fwd(AttnArgs a) {
       s[sub] = f32x16{};
 #pragma unroll
       for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(&Ks[sub * 32 + l32][16 * kk + 8 * half]);
+        const bf16x8 kf = *reinterpret_cast<const bf16x8 *>(&Ks[b][sub * 32 + l32][16 * kk + 8 * half]);
         s[sub] = mfma32(kf, qf[kk], s[sub]);
       }
     }
-    float mt = -INFINITY;
+    if constexpr (decltype(masked)::value) {
+#pragma unroll
+      for (int sub = 0; sub < 2; ++sub) {
+#pragma unroll
+        for (int jj = 0; jj < 16; ++jj) {
+          const int key = k0 + sub * 32 + 8 * (jj >> 2) + 4 * half + (jj & 3);
+          if (key > vis) s[sub][jj] = -INFINITY;
+        }
+      }
+    }
+    float mx = -INFINITY;
 #pragma unroll
     for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
-      for (int jj = 0; jj < 16; ++jj) {
-        const int key = k0 + sub * 32 + 8 * (jj >> 2) + 4 * half + (jj & 3);
-        const float x = key <= vis ? s[sub][jj] * c : -INFINITY;
-        s[sub][jj] = x;
-        mt = fmaxf(mt, x);
-      }
+      for (int jj = 0; jj < 16; ++jj) mx = fmaxf(mx, s[sub][jj]);
     }
-    mt = fmaxf(mt, __shfl_xor(mt, 32));
-    const float m_new = fmaxf(m_run, mt);
-    const float alpha = fast_exp2(m_run - m_new);
-    m_run = m_new;
-    l_run *= alpha;
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mt = mx * c;
+    // Lazy rescaling: the running maximum only moves when a row's tile
+    // maximum exceeds it by more than 2^8, so probabilities stay <= 256.
+    if (__any(mt > m_run + 8.f)) {
+      const float m_new = fmaxf(m_run, mt);
+      const float alpha = fast_exp2(m_run - m_new);
+      m_run = m_new;
+      l_run *= alpha;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
+      for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
+    }
 
     bf16x8 pf[4];
     float ls = 0.f;
@@ -161,27 +217,44 @@ __global__ __launch_bounds__(256) void attn_fwd(AttnArgs a) {
     for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
       for (int jj = 0; jj < 16; ++jj) {
-        const float p = fast_exp2(s[sub][jj] - m_new);
+        const float p = fast_exp2(fmaf(s[sub][jj], c, -m_run));
         ls += p;
         pf[2 * sub + (jj >> 3)][jj & 7] = static_cast<__bf16>(p);
       }
     }
     l_run += ls;
 
-    // O^T += V^T P^T: B element t of lane half hf in key group qq is key
-    // 16 qq + 8 (t/4) + 4 hf + t%4, so A reads V^T at the same keys.
+    // O^T += V^T P^T.  B element t of lane half hf in key group qq is key
+    // 16 qq + 8 (t/4) + 4 hf + t%4; two transposed reads give the matching
+    // V^T fragment (keys 16 qq + 4 hf + 0..3 and 16 qq + 8 + 4 hf + 0..3).
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      const uint16_t *vrow = &Vt[32 * db + l32][0];
 #pragma unroll
       for (int qq = 0; qq < 4; ++qq) {
-        const uint2 lo = *reinterpret_cast<const uint2 *>(vrow + 16 * qq + 4 * half);
-        const uint2 hi = *reinterpret_cast<const uint2 *>(vrow + 16 * qq + 8 + 4 * half);
-        const uint4 packed = {lo.x, lo.y, hi.x, hi.y};
-        const bf16x8 vf = __builtin_bit_cast(bf16x8, packed);
+        const uint16_t *vp = &Vs[b][16 * qq + tr_row][32 * db + tr_col];
+        const s4 lo = lds_tr16(vp);
+        const s4 hi = lds_tr16(vp + 8 * (D + VPAD));
+        const bf16x8 vf = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
         o[db] = mfma32(vf, pf[qq], o[db]);
       }
     }
+  };
+
+  using NoMask = std::integral_constant<bool, false>;
+  using Mask = std::integral_constant<bool, true>;
+  if (n_pure > 0) load_pure(0); else load_any(0);
+  for (int t = 0; t < n_pure; ++t) {
+    store_tile(t & 1);
+    __syncthreads();
+    if (t + 1 < n_pure) load_pure((t + 1) * BN);
+    else if (t + 1 < ntiles) load_any((t + 1) * BN);
+    compute(t, NoMask{});
+  }
+  for (int t = n_pure; t < ntiles; ++t) {
+    store_tile(t & 1);
+    __syncthreads();
+    if (t + 1 < ntiles) load_any((t + 1) * BN);
+    if ((t + 1) * BN - 1 > vis_min) compute(t, Mask{}); else compute(t, NoMask{});
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
@@ -222,10 +295,17 @@ __global__ __launch_bounds__(256) void attn_colsum(ColsumArgs a) {
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int half = lane >> 5, l32 = lane & 31;
-  const int key = k0 + wave * 32 + l32;          // column n of this lane
-  const bool key_ok = key < T;
-  const int pmin_key = key < T0 ? 0 : (key - T0) * G;
+  // Each wave owns 64 candidates (two MFMA columns blocks of 32).
+  const int kw0 = k0 + wave * 64;
+  int key[2], pmin[2];
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    key[kb] = kw0 + 32 * kb + l32;
+    pmin[kb] = key[kb] < T0 ? 0 : (key[kb] - T0) * G;   // first packed row that sees it
+  }
+  const bool wave_masked = kw0 + 63 >= T0;            // holds chunk candidates or the tail
   const int p_begin = (k0 < T0 ? 0 : (k0 - T0) * G) & ~(BQ - 1);
+  const int ntq = (P - p_begin + BQ - 1) / BQ;
 
   const int slot = a.slot[j];
   const uint16_t *q = a.q + slot * a.q_lstride;
@@ -233,64 +313,110 @@ __global__ __launch_bounds__(256) void attn_colsum(ColsumArgs a) {
   const uint16_t *kc = lt.k[cur];
   const float c = a.scale_log2;
 
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[BQ][D + KPAD];
-  __shared__ __attribute__((aligned(16))) float Ls[BQ];
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[2][BQ][D + KPAD];
+  __shared__ __attribute__((aligned(16))) float Ls[2][BQ];
 
-  double wacc = 0.0;
-  for (int kv = 0; kv < Hkv; ++kv) {
-    bf16x8 kf[D / 16];
-    const uint16_t *krow = key < T0 ? kc + ((int64_t)key * Hkv + kv) * D
-                                    : kn + ((int64_t)(key - T0) * Hkv + kv) * D;
+  constexpr int CH = D / 8;
+  constexpr int NLD = BQ * CH / 256;
+  uint4 qreg[NLD];
+  float lreg = INFINITY;
+  auto load_tile = [&](int it) {
+    const int kv = it / ntq;
+    const int pt = p_begin + (it - kv * ntq) * BQ;
 #pragma unroll
-    for (int kk = 0; kk < D / 16; ++kk) {
-      kf[kk] = key_ok ? *reinterpret_cast<const bf16x8 *>(krow + 16 * kk + 8 * half) : bf16x8{};
-    }
-    const float *lse = a.lse + layer * a.lse_lstride + (int64_t)kv * P;
-
-    for (int pt = p_begin; pt < P; pt += BQ) {
-      __syncthreads();
-      constexpr int CH = D / 8;
-      for (int e = tid; e < BQ * CH; e += 256) {
-        const int rr = e / CH, ch = e - (e / CH) * CH;
-        const int p = pt + rr;
-        uint4 v = {0u, 0u, 0u, 0u};
-        if (p < P) {
-          const int r = p / G, g = p - (p / G) * G;
-          v = *reinterpret_cast<const uint4 *>(q + ((int64_t)r * Hq + kv * G + g) * D + ch * 8);
-        }
-        *reinterpret_cast<uint4 *>(&Qs[rr][ch * 8]) = v;
+    for (int u = 0; u < NLD; ++u) {
+      const int e = tid + u * 256;
+      const int rr = e / CH, ch = e % CH;
+      const int p = pt + rr;
+      uint4 v = {0u, 0u, 0u, 0u};
+      if (p < P) {
+        const int r = p / G, g = p - (p / G) * G;
+        v = gload16(q + ((int64_t)r * Hq + kv * G + g) * D + ch * 8);
       }
-      if (tid < BQ) Ls[tid] = (pt + tid < P) ? lse[pt + tid] : INFINITY;
-      __syncthreads();
+      qreg[u] = v;
+    }
+    if (tid < BQ) {
+      const float *lse = a.lse + layer * a.lse_lstride + (int64_t)kv * P;
+      lreg = (pt + tid < P) ? lse[pt + tid] : INFINITY;
+    }
+  };
+  auto store_tile = [&](int b) {
+#pragma unroll
+    for (int u = 0; u < NLD; ++u) {
+      const int e = tid + u * 256;
+      const int rr = e / CH, ch = e % CH;
+      *reinterpret_cast<uint4 *>(&Qs[b][rr][ch * 8]) = qreg[u];
+    }
+    if (tid < BQ) Ls[b][tid] = lreg;
+  };
+
+  double wacc[2] = {0.0, 0.0};
+  bf16x8 kf[2][D / 16];
+  int kv_loaded = -1;
+  const int nit = Hkv * ntq;
+  load_tile(0);
+  for (int it = 0; it < nit; ++it) {
+    const int b = it & 1;
+    const int kv = it / ntq;
+    const int pt = p_begin + (it - kv * ntq) * BQ;
+    store_tile(b);
+    if (kv != kv_loaded) {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        const bool ok = key[kb] < T;
+        const uint16_t *krow = key[kb] < T0 ? kc + ((int64_t)key[kb] * Hkv + kv) * D
+                                            : kn + ((int64_t)(key[kb] - T0) * Hkv + kv) * D;
+#pragma unroll
+        for (int kk = 0; kk < D / 16; ++kk)
+          kf[kb][kk] = ok ? __builtin_bit_cast(bf16x8, gload16(krow + 16 * kk + 8 * half)) : bf16x8{};
+      }
+      kv_loaded = kv;
+    }
+    __syncthreads();
+    if (it + 1 < nit) load_tile(it + 1);
 
 #pragma unroll
-      for (int rb = 0; rb < BQ / 32; ++rb) {
-        // S = Q K^T: lane = candidate, register = query row.
-        f32x16 s = f32x16{};
+    for (int rb = 0; rb < BQ / 32; ++rb) {
+      // S = Q K^T: lane = candidate, register = query row.
+      f32x16 s[2] = {f32x16{}, f32x16{}};
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk) {
-          const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[rb * 32 + l32][16 * kk + 8 * half]);
-          s = mfma32(qv, kf[kk], s);
-        }
+      for (int kk = 0; kk < D / 16; ++kk) {
+        const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[b][rb * 32 + l32][16 * kk + 8 * half]);
+        s[0] = mfma32(qv, kf[0][kk], s[0]);
+        s[1] = mfma32(qv, kf[1][kk], s[1]);
+      }
+      float lv[16];
+#pragma unroll
+      for (int grp = 0; grp < 4; ++grp) {
+        const float4 l4 = *reinterpret_cast<const float4 *>(&Ls[b][rb * 32 + 8 * grp + 4 * half]);
+        lv[4 * grp + 0] = l4.x;
+        lv[4 * grp + 1] = l4.y;
+        lv[4 * grp + 2] = l4.z;
+        lv[4 * grp + 3] = l4.w;
+      }
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
         float ts = 0.f;
+        if (wave_masked) {
 #pragma unroll
-        for (int grp = 0; grp < 4; ++grp) {
-          const int rloc = rb * 32 + 8 * grp + 4 * half;
-          const float4 l4 = *reinterpret_cast<const float4 *>(&Ls[rloc]);
-          const float lv[4] = {l4.x, l4.y, l4.z, l4.w};
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const float x = fmaf(s[4 * grp + e], c, -lv[e]);
-            const float p = fast_exp2(x);
-            ts += (pt + rloc + e >= pmin_key) ? p : 0.f;
+          for (int e = 0; e < 16; ++e) {
+            const int prow = pt + rb * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
+            const float p = fast_exp2(fmaf(s[kb][e], c, -lv[e]));
+            ts += prow >= pmin[kb] ? p : 0.f;
           }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 16; ++e) ts += fast_exp2(fmaf(s[kb][e], c, -lv[e]));
         }
-        wacc += (double)ts;
+        wacc[kb] += (double)ts;
       }
     }
   }
-  wacc += __shfl_xor(wacc, 32);
-  if (key_ok && half == 0) lt.w[key] = (float)wacc;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb) {
+    const double wsum = wacc[kb] + __shfl_xor(wacc[kb], 32);
+    if (key[kb] < T && half == 0) lt.w[key[kb]] = (float)wsum;
+  }
 }
 
 }  // namespace

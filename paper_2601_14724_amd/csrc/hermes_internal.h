@@ -110,6 +110,6 @@ hipError_t launch_topk(const float *keys, int n, int k, int32_t *out, hipStream_
 
 // Geometry shared by host sizing and kernels.
 constexpr int kAttnRowsPerBlock = 128;   // packed (row, head) pairs per workgroup
-constexpr int kColsumKeysPerBlock = 128; // candidates per workgroup of the sweep
+constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the sweep
 
 }  // namespace hermes
