@@ -28,7 +28,7 @@ typedef short s4 __attribute__((ext_vector_type(4)));
 constexpr int BM = kAttnRowsPerBlock;    // packed rows per workgroup (4 waves x 32)
 constexpr int BN = 64;                   // keys per tile
 constexpr int BK = kColsumKeysPerBlock;  // candidates per sweep workgroup (4 waves x 64)
-constexpr int BQ = 64;                   // packed rows per sweep tile
+constexpr int BQS = 32;                  // packed rows per sweep tile
 constexpr int KPAD = 8;                  // u16 padding of K / Q rows in LDS
 constexpr int VPAD = 16;                 // u16 padding of V rows in LDS
 
@@ -280,7 +280,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256) void attn_colsum(ColsumArgs a) {
+__global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
   const int j = blockIdx.z;
   const int layer = a.layer_id[j];
   const LayerTable &lt = a.tab[layer];
@@ -295,7 +295,7 @@ __global__ __launch_bounds__(256) void attn_colsum(ColsumArgs a) {
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int half = lane >> 5, l32 = lane & 31;
-  // Each wave owns 64 candidates (two MFMA columns blocks of 32).
+  // Each wave owns 64 candidates (two MFMA column blocks of 32).
   const int kw0 = k0 + wave * 64;
   int key[2], pmin[2];
 #pragma unroll
@@ -303,120 +303,165 @@ __global__ __launch_bounds__(256) void attn_colsum(ColsumArgs a) {
     key[kb] = kw0 + 32 * kb + l32;
     pmin[kb] = key[kb] < T0 ? 0 : (key[kb] - T0) * G;   // first packed row that sees it
   }
-  const bool wave_masked = kw0 + 63 >= T0;            // holds chunk candidates or the tail
-  const int p_begin = (k0 < T0 ? 0 : (k0 - T0) * G) & ~(BQ - 1);
-  const int ntq = (P - p_begin + BQ - 1) / BQ;
+  // rows below pmask_end may be invisible to some candidate of this wave
+  const int pmask_end = kw0 + 63 < T0 ? 0 : (kw0 + 63 - T0) * G + 1;
+  const int p_begin = (k0 < T0 ? 0 : (k0 - T0) * G) & ~(BQS - 1);
+  const int ntq = (P - p_begin + BQS - 1) / BQS;
+  const int nit = ntq;
+  const int kv_blk = blockIdx.y;   // one KV head per workgroup; heads are summed afterwards
 
   const int slot = a.slot[j];
   const uint16_t *q = a.q + slot * a.q_lstride;
   const uint16_t *kn = a.kn + slot * a.kv_lstride;
   const uint16_t *kc = lt.k[cur];
+  const float *lse_l = a.lse + layer * a.lse_lstride;
   const float c = a.scale_log2;
 
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[2][BQ][D + KPAD];
-  __shared__ __attribute__((aligned(16))) float Ls[2][BQ];
+  // Three-deep ring of 32-row query tiles: tile it+1 is read by the MFMAs
+  // while tile it's probabilities are summed and tile it+2 is stored.
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[3][BQS][D + KPAD];
+  __shared__ __attribute__((aligned(16))) float Ls[3][BQS];
 
   constexpr int CH = D / 8;
-  constexpr int NLD = BQ * CH / 256;
+  constexpr int NLD = BQS * CH / 256;
   uint4 qreg[NLD];
   float lreg = INFINITY;
+  auto tile_kv = [&](int) { return kv_blk; };
+  auto tile_p = [&](int it) { return p_begin + it * BQS; };
   auto load_tile = [&](int it) {
-    const int kv = it / ntq;
-    const int pt = p_begin + (it - kv * ntq) * BQ;
+    const int kv = tile_kv(it), pt = tile_p(it);
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
       const int e = tid + u * 256;
-      const int rr = e / CH, ch = e % CH;
-      const int p = pt + rr;
+      const int p = pt + e / CH;
       uint4 v = {0u, 0u, 0u, 0u};
       if (p < P) {
         const int r = p / G, g = p - (p / G) * G;
-        v = gload16(q + ((int64_t)r * Hq + kv * G + g) * D + ch * 8);
+        v = gload16(q + ((int64_t)r * Hq + kv * G + g) * D + (e % CH) * 8);
       }
       qreg[u] = v;
     }
-    if (tid < BQ) {
-      const float *lse = a.lse + layer * a.lse_lstride + (int64_t)kv * P;
-      lreg = (pt + tid < P) ? lse[pt + tid] : INFINITY;
-    }
+    if (tid < BQS) lreg = (pt + tid < P) ? lse_l[(int64_t)kv * P + pt + tid] : INFINITY;
   };
-  auto store_tile = [&](int b) {
+  auto store_tile = [&](int it) {
+    const int b = it % 3;
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
       const int e = tid + u * 256;
-      const int rr = e / CH, ch = e % CH;
-      *reinterpret_cast<uint4 *>(&Qs[b][rr][ch * 8]) = qreg[u];
+      *reinterpret_cast<uint4 *>(&Qs[b][e / CH][(e % CH) * 8]) = qreg[u];
     }
-    if (tid < BQ) Ls[b][tid] = lreg;
+    if (tid < BQS) Ls[b][tid] = lreg;
   };
 
-  double wacc[2] = {0.0, 0.0};
   bf16x8 kf[2][D / 16];
   int kv_loaded = -1;
-  const int nit = Hkv * ntq;
-  load_tile(0);
-  for (int it = 0; it < nit; ++it) {
-    const int b = it & 1;
-    const int kv = it / ntq;
-    const int pt = p_begin + (it - kv * ntq) * BQ;
-    store_tile(b);
-    if (kv != kv_loaded) {
+  auto load_keys = [&](int kv) {
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        const bool ok = key[kb] < T;
-        const uint16_t *krow = key[kb] < T0 ? kc + ((int64_t)key[kb] * Hkv + kv) * D
-                                            : kn + ((int64_t)(key[kb] - T0) * Hkv + kv) * D;
+    for (int kb = 0; kb < 2; ++kb) {
+      const bool ok = key[kb] < T;
+      const uint16_t *krow = key[kb] < T0 ? kc + ((int64_t)key[kb] * Hkv + kv) * D
+                                          : kn + ((int64_t)(key[kb] - T0) * Hkv + kv) * D;
 #pragma unroll
-        for (int kk = 0; kk < D / 16; ++kk)
-          kf[kb][kk] = ok ? __builtin_bit_cast(bf16x8, gload16(krow + 16 * kk + 8 * half)) : bf16x8{};
-      }
-      kv_loaded = kv;
+      for (int kk = 0; kk < D / 16; ++kk)
+        kf[kb][kk] = ok ? __builtin_bit_cast(bf16x8, gload16(krow + 16 * kk + 8 * half)) : bf16x8{};
     }
-    __syncthreads();
-    if (it + 1 < nit) load_tile(it + 1);
-
+    kv_loaded = kv;
+  };
+  // S = Q K^T for one 32-row tile: lane = candidate, register = query row.
+  auto scores = [&](int it, f32x16 *s) {
+    const int b = it % 3;
+    s[0] = f32x16{};
+    s[1] = f32x16{};
 #pragma unroll
-    for (int rb = 0; rb < BQ / 32; ++rb) {
-      // S = Q K^T: lane = candidate, register = query row.
-      f32x16 s[2] = {f32x16{}, f32x16{}};
+    for (int kk = 0; kk < D / 16; ++kk) {
+      const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[b][l32][16 * kk + 8 * half]);
+      s[0] = mfma32(qv, kf[0][kk], s[0]);
+      s[1] = mfma32(qv, kf[1][kk], s[1]);
+    }
+  };
+  double wacc[2] = {0.0, 0.0};
+  auto accumulate = [&](int it, const f32x16 *s) {
+    const int b = it % 3;
+    const int pt = tile_p(it);
+    float lv[16];
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk) {
-        const bf16x8 qv = *reinterpret_cast<const bf16x8 *>(&Qs[b][rb * 32 + l32][16 * kk + 8 * half]);
-        s[0] = mfma32(qv, kf[0][kk], s[0]);
-        s[1] = mfma32(qv, kf[1][kk], s[1]);
-      }
-      float lv[16];
-#pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        const float4 l4 = *reinterpret_cast<const float4 *>(&Ls[b][rb * 32 + 8 * grp + 4 * half]);
-        lv[4 * grp + 0] = l4.x;
-        lv[4 * grp + 1] = l4.y;
-        lv[4 * grp + 2] = l4.z;
-        lv[4 * grp + 3] = l4.w;
-      }
+    for (int grp = 0; grp < 4; ++grp) {
+      const float4 l4 = *reinterpret_cast<const float4 *>(&Ls[b][8 * grp + 4 * half]);
+      lv[4 * grp + 0] = l4.x;
+      lv[4 * grp + 1] = l4.y;
+      lv[4 * grp + 2] = l4.z;
+      lv[4 * grp + 3] = l4.w;
+    }
+    if (pt < pmask_end) {   // causal edge of this wave's chunk candidates
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
         float ts = 0.f;
-        if (wave_masked) {
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            const int prow = pt + rb * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-            const float p = fast_exp2(fmaf(s[kb][e], c, -lv[e]));
-            ts += prow >= pmin[kb] ? p : 0.f;
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 16; ++e) ts += fast_exp2(fmaf(s[kb][e], c, -lv[e]));
+        for (int e = 0; e < 16; ++e) {
+          const int prow = pt + 8 * (e >> 2) + 4 * half + (e & 3);
+          const float p = fast_exp2(fmaf(s[kb][e], c, -lv[e]));
+          ts += prow >= pmin[kb] ? p : 0.f;
         }
         wacc[kb] += (double)ts;
       }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb) {
+        float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+        for (int e = 0; e < 16; e += 2) {
+          t0 += fast_exp2(fmaf(s[kb][e], c, -lv[e]));
+          t1 += fast_exp2(fmaf(s[kb][e + 1], c, -lv[e + 1]));
+        }
+        wacc[kb] += (double)(t0 + t1);
+      }
     }
+  };
+
+  load_tile(0);
+  store_tile(0);
+  if (nit > 1) {
+    load_tile(1);
+    store_tile(1);
   }
+  if (nit > 2) load_tile(2);
+  load_keys(tile_kv(0));
+  __syncthreads();
+  f32x16 s_cur[2], s_nxt[2];
+  scores(0, s_cur);
+  for (int it = 0; it < nit; ++it) {
+    if (it + 1 < nit) {
+      if (tile_kv(it + 1) != kv_loaded) load_keys(tile_kv(it + 1));
+      scores(it + 1, s_nxt);
+    }
+    accumulate(it, s_cur);
+    if (it + 2 < nit) {
+      store_tile(it + 2);
+      if (it + 3 < nit) load_tile(it + 3);
+    }
+    __syncthreads();
+    s_cur[0] = s_nxt[0];
+    s_cur[1] = s_nxt[1];
+  }
+  double *part = a.wpart + layer * a.wpart_lstride + (int64_t)kv_blk * a.wpart_hstride;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
     const double wsum = wacc[kb] + __shfl_xor(wacc[kb], 32);
-    if (key[kb] < T && half == 0) lt.w[key[kb]] = (float)wsum;
+    if (key[kb] < T && half == 0) part[key[kb]] = wsum;
   }
+}
+
+// W_i = sum over KV heads of the per-head partial masses, in head order.
+__global__ __launch_bounds__(256) void mass_reduce(ColsumArgs a) {
+  const int j = blockIdx.y;
+  const int layer = a.layer_id[j];
+  const int T = a.T0[j] + a.C;
+  const int i = blockIdx.x * 256 + threadIdx.x;
+  if (i >= T) return;
+  const double *part = a.wpart + layer * a.wpart_lstride + i;
+  double w = 0.0;
+  for (int kv = 0; kv < a.Hkv; ++kv) w += part[(int64_t)kv * a.wpart_hstride];
+  a.tab[layer].w[i] = (float)w;
 }
 
 }  // namespace
@@ -434,12 +479,15 @@ hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStre
 
 hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_dim,
                          hipStream_t s) {
-  dim3 grid((max_T + BK - 1) / BK, 1, n_list);
+  dim3 grid((max_T + BK - 1) / BK, a.Hkv, n_list);
   if (head_dim == 64) {
     hipLaunchKernelGGL(attn_colsum<64>, grid, dim3(256), 0, s, a);
   } else {
     hipLaunchKernelGGL(attn_colsum<128>, grid, dim3(256), 0, s, a);
   }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(mass_reduce, dim3((max_T + 255) / 256, n_list), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

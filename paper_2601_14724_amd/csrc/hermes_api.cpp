@@ -23,8 +23,8 @@ size_t round_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t tab, lse, keys, kept, total;
-  int64_t lse_lstride, keys_lstride, kept_lstride;
+  size_t tab, lse, keys, kept, wpart, total;
+  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride;
 };
 
 int max_budget(const hermes_config *c) {
@@ -73,6 +73,9 @@ Layout layout_of(const hermes_config *c) {
   off = round_up(off + sizeof(uint32_t) * (size_t)s.keys_lstride * c->n_layers);
   s.kept = off;
   off = round_up(off + sizeof(int32_t) * (size_t)s.kept_lstride * c->n_layers);
+  s.wpart_lstride = (int64_t)c->n_kv_heads * c->max_cap;
+  s.wpart = off;
+  off = round_up(off + sizeof(double) * (size_t)s.wpart_lstride * c->n_layers);
   s.total = off;
   return s;
 }
@@ -386,6 +389,9 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   cs.kn = ap.kn;
   cs.vn = ap.vn;
   cs.lse = at.lse;
+  cs.wpart = reinterpret_cast<double *>(ctx->ws + ctx->lay.wpart);
+  cs.wpart_lstride = ctx->lay.wpart_lstride;
+  cs.wpart_hstride = ctx->max_cap;
   cs.q_lstride = q_ls;
   cs.kv_lstride = kv_ls;
   cs.lse_lstride = at.lse_lstride;

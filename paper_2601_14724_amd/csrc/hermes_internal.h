@@ -44,12 +44,15 @@ struct AttnArgs {
   int8_t cur[kMaxLayers];
 };
 
-// Attention-mass sweep: W_i for every candidate of layer layer_id[j].
+// Attention-mass sweep: W_i for every candidate of layer layer_id[j].  Each
+// KV head's share goes to wpart[layer][kv][i] (fp64), then is summed into
+// the layer's w buffer in head order.
 struct ColsumArgs {
   const LayerTable *tab;
   const uint16_t *q, *kn, *vn;
   const float *lse;
-  int64_t q_lstride, kv_lstride, lse_lstride;
+  double *wpart;
+  int64_t q_lstride, kv_lstride, lse_lstride, wpart_lstride, wpart_hstride;
   int32_t Hq, Hkv, C;
   float scale_log2;
   int32_t T0[kMaxLayers];

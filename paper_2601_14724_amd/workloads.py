@@ -205,9 +205,12 @@ def custom(name: str, workload_id: int, n_layers: int, n_q_heads: int, n_kv_head
                     scale)
 
 
-def stack_chunks(wl: Workload, step: int, layers: Optional[Sequence[int]] = None) -> dict:
+def stack_chunks(wl: Workload, step: int, layers: Optional[Sequence[int]] = None,
+                 threads: int = 8) -> dict:
     """All layers' chunk inputs stacked on a leading layer axis."""
-    layers = range(wl.n_layers) if layers is None else layers
-    parts = [gen_chunk(wl, step, l) for l in layers]
+    import concurrent.futures as cf
+    layers = list(range(wl.n_layers) if layers is None else layers)
+    with cf.ThreadPoolExecutor(max_workers=max(1, threads)) as ex:
+        parts = list(ex.map(lambda l: gen_chunk(wl, step, l), layers))
     return {key: np.stack([p[key] for p in parts]) for key in ("q", "k", "v")} | {
         "pos": parts[0]["pos"]}

@@ -116,3 +116,33 @@ def check_layer(l, kv, out_gpu, w_gpu, ref, budget, chunk, check_w=True, check_s
 def raw_bits(caches, chunks):
     return {"cache_k": [c["k"] for c in caches], "cache_v": [c["v"] for c in caches],
             "chunk_k": [c["k"] for c in chunks], "chunk_v": [c["v"] for c in chunks]}
+
+
+# ---------------------------------------------------------------------------
+# per-layer oracle composition for full-size workloads (sampled layers)
+# ---------------------------------------------------------------------------
+
+def oracle_layer_attention(cache, chunk):
+    """Oracle O and W of one layer (cache/chunk as generated bit patterns)."""
+    return orc.chunk_attention(f64(chunk["q"]), f64(cache["k"]), f64(cache["v"]),
+                               f64(chunk["k"]), f64(chunk["v"]))
+
+
+def oracle_layer_score(l, classes, w, T0, C, forget_rate=orc.DEFAULT_FORGET_RATE, alpha_mode=0):
+    """Raw importance S^l from the oracle's scoring functions (Sec. 3.1)."""
+    T = T0 + C
+    r = orc.recency_importance(T, forget_rate)
+    a = orc.attention_importance(w, T0, C, alpha_mode) if classes[l] != orc.SHALLOW else None
+    om = orc.omega(l, classes) if classes[l] == orc.MIDDLE else 0.0
+    return orc.raw_importance(classes[l], om, a, r)
+
+
+def check_kept(idx_gpu, st, budget, what):
+    """Kept sets bit-exact except inside the 1e-6 band of the budget-th score."""
+    idx_ref = orc.topk_indices(st, budget)
+    assert len(idx_gpu) == budget and np.all(np.diff(idx_gpu) > 0), f"{what}: bad index list"
+    diff = np.setxor1d(idx_gpu, idx_ref)
+    band = band_of(st, budget)
+    outside = [int(i) for i in diff if not band[i]]
+    assert not outside, f"{what}: kept sets differ outside the 1e-6 band at {outside[:10]}"
+    return len(diff)
