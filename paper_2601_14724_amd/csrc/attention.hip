@@ -30,7 +30,7 @@ constexpr int BN = 64;                   // keys per tile
 constexpr int BK = kColsumKeysPerBlock;  // candidates per sweep workgroup (4 waves x 64)
 constexpr int BQS = 32;                  // packed rows per sweep tile
 constexpr int KPAD = 8;                  // u16 padding of K / Q rows in LDS
-constexpr int VPAD = 16;                 // u16 padding of V rows in LDS
+constexpr int VPAD = 32;                 // u16 padding of V rows in LDS
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -41,6 +41,7 @@ __device__ __forceinline__ uint16_t f2bf(float x) {
 }
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
 
 // 16-byte load through the global (not flat) address space, so outstanding
 // prefetches are tracked by vmcnt only and never delay LDS waits.
@@ -57,10 +58,21 @@ __device__ __forceinline__ s4 lds_tr16(const uint16_t *p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s4 *)p);
 }
 
+// Workgroups are dispatched to the 8 XCDs round-robin by linear id; this
+// maps linear ids so that consecutive logical tiles (the q-tiles of one
+// layer and KV head, which stream the same K/V) run on the same XCD and
+// share its L2.
+__device__ __forceinline__ int xcd_remap(int i, int n) {
+  const int q = n / 8, r = n % 8, x = i % 8, k = i / 8;
+  return x < r ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
+}
+
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a) {
-  const int j = blockIdx.z;
-  const int kv = blockIdx.y;
+__global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int qtile = lin % nqt;
+  const int kv = (lin / nqt) % a.Hkv;
+  const int j = lin / (nqt * a.Hkv);
   const int layer = a.layer_id[j];
   const LayerTable &lt = a.tab[layer];
   const int cur = a.cur[j];
@@ -69,7 +81,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a) {
   const int G = Hq / Hkv;
   const int P = C * G;
   const int T = T0 + C;
-  const int p0 = blockIdx.x * BM;
+  const int p0 = qtile * BM;
   if (p0 >= P) return;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -279,9 +291,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a) {
   }
 }
 
+
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
-  const int j = blockIdx.z;
+__global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
+  const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  const int kblk = lin % nkb;
+  const int kv_blk = (lin / nkb) % a.Hkv;
+  const int j = lin / (nkb * a.Hkv);
   const int layer = a.layer_id[j];
   const LayerTable &lt = a.tab[layer];
   const int cur = a.cur[j];
@@ -290,7 +306,7 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
   const int G = Hq / Hkv;
   const int P = C * G;
   const int T = T0 + C;
-  const int k0 = blockIdx.x * BK;
+  const int k0 = kblk * BK;
   if (k0 >= T) return;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
@@ -308,7 +324,6 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
   const int p_begin = (k0 < T0 ? 0 : (k0 - T0) * G) & ~(BQS - 1);
   const int ntq = (P - p_begin + BQS - 1) / BQS;
   const int nit = ntq;
-  const int kv_blk = blockIdx.y;   // one KV head per workgroup; heads are summed afterwards
 
   const int slot = a.slot[j];
   const uint16_t *q = a.q + slot * a.q_lstride;
@@ -354,19 +369,15 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
   };
 
   bf16x8 kf[2][D / 16];
-  int kv_loaded = -1;
-  auto load_keys = [&](int kv) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      const bool ok = key[kb] < T;
-      const uint16_t *krow = key[kb] < T0 ? kc + ((int64_t)key[kb] * Hkv + kv) * D
-                                          : kn + ((int64_t)(key[kb] - T0) * Hkv + kv) * D;
+  for (int kb = 0; kb < 2; ++kb) {
+    const bool ok = key[kb] < T;
+    const uint16_t *krow = key[kb] < T0 ? kc + ((int64_t)key[kb] * Hkv + kv_blk) * D
+                                        : kn + ((int64_t)(key[kb] - T0) * Hkv + kv_blk) * D;
 #pragma unroll
-      for (int kk = 0; kk < D / 16; ++kk)
-        kf[kb][kk] = ok ? __builtin_bit_cast(bf16x8, gload16(krow + 16 * kk + 8 * half)) : bf16x8{};
-    }
-    kv_loaded = kv;
-  };
+    for (int kk = 0; kk < D / 16; ++kk)
+      kf[kb][kk] = ok ? __builtin_bit_cast(bf16x8, gload16(krow + 16 * kk + 8 * half)) : bf16x8{};
+  }
   // S = Q K^T for one 32-row tile: lane = candidate, register = query row.
   auto scores = [&](int it, f32x16 *s) {
     const int b = it % 3;
@@ -380,10 +391,8 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
     }
   };
   double wacc[2] = {0.0, 0.0};
-  auto accumulate = [&](int it, const f32x16 *s) {
+  auto read_lse = [&](int it, float *lv) {
     const int b = it % 3;
-    const int pt = tile_p(it);
-    float lv[16];
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp) {
       const float4 l4 = *reinterpret_cast<const float4 *>(&Ls[b][8 * grp + 4 * half]);
@@ -392,31 +401,35 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
       lv[4 * grp + 2] = l4.z;
       lv[4 * grp + 3] = l4.w;
     }
-    if (pt < pmask_end) {   // causal edge of this wave's chunk candidates
+  };
+  auto acc_masked = [&](int it, const f32x16 *s, const float *lv) {
+    const int pt = tile_p(it);
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        float ts = 0.f;
+    for (int kb = 0; kb < 2; ++kb) {
+      float ts = 0.f;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int prow = pt + 8 * (e >> 2) + 4 * half + (e & 3);
-          const float p = fast_exp2(fmaf(s[kb][e], c, -lv[e]));
-          ts += prow >= pmin[kb] ? p : 0.f;
-        }
-        wacc[kb] += (double)ts;
+      for (int e = 0; e < 16; ++e) {
+        const int prow = pt + 8 * (e >> 2) + 4 * half + (e & 3);
+        const float p = fast_exp2(fmaf(s[kb][e], c, -lv[e]));
+        ts += prow >= pmin[kb] ? p : 0.f;
       }
-    } else {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
-        float t0 = 0.f, t1 = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; e += 2) {
-          t0 += fast_exp2(fmaf(s[kb][e], c, -lv[e]));
-          t1 += fast_exp2(fmaf(s[kb][e + 1], c, -lv[e + 1]));
-        }
-        wacc[kb] += (double)(t0 + t1);
-      }
+      wacc[kb] += (double)ts;
     }
   };
+  auto acc_plain = [&](const f32x16 *s, const float *lv) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      float t0 = 0.f, t1 = 0.f;
+#pragma unroll
+      for (int e = 0; e < 16; e += 2) {
+        t0 += fast_exp2(fmaf(s[kb][e], c, -lv[e]));
+        t1 += fast_exp2(fmaf(s[kb][e + 1], c, -lv[e + 1]));
+      }
+      wacc[kb] += (double)(t0 + t1);
+    }
+  };
+  // tiles [0, n_mask) touch the causal edge of this wave's candidates
+  const int n_mask = min(nit, max(0, (pmask_end - p_begin + BQS - 1) / BQS));
 
   load_tile(0);
   store_tile(0);
@@ -425,16 +438,14 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
     store_tile(1);
   }
   if (nit > 2) load_tile(2);
-  load_keys(tile_kv(0));
   __syncthreads();
   f32x16 s_cur[2], s_nxt[2];
   scores(0, s_cur);
-  for (int it = 0; it < nit; ++it) {
-    if (it + 1 < nit) {
-      if (tile_kv(it + 1) != kv_loaded) load_keys(tile_kv(it + 1));
-      scores(it + 1, s_nxt);
-    }
-    accumulate(it, s_cur);
+  auto step = [&](int it, auto masked) {
+    float lv[16];
+    if (it + 1 < nit) scores(it + 1, s_nxt);
+    read_lse(it, lv);
+    if constexpr (decltype(masked)::value) acc_masked(it, s_cur, lv); else acc_plain(s_cur, lv);
     if (it + 2 < nit) {
       store_tile(it + 2);
       if (it + 3 < nit) load_tile(it + 3);
@@ -442,7 +453,22 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a) {
     __syncthreads();
     s_cur[0] = s_nxt[0];
     s_cur[1] = s_nxt[1];
+  };
+  int it = 0;
+  for (; it < n_mask; ++it) step(it, std::integral_constant<bool, true>{});
+  // steady state: no branches inside the body
+  for (; it + 3 < nit; ++it) {
+    float lv[16];
+    scores(it + 1, s_nxt);
+    read_lse(it, lv);
+    acc_plain(s_cur, lv);
+    store_tile(it + 2);
+    load_tile(it + 3);
+    __syncthreads();
+    s_cur[0] = s_nxt[0];
+    s_cur[1] = s_nxt[1];
   }
+  for (; it < nit; ++it) step(it, std::integral_constant<bool, false>{});
   double *part = a.wpart + layer * a.wpart_lstride + (int64_t)kv_blk * a.wpart_hstride;
 #pragma unroll
   for (int kb = 0; kb < 2; ++kb) {
@@ -468,22 +494,24 @@ __global__ __launch_bounds__(256) void mass_reduce(ColsumArgs a) {
 
 hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStream_t s) {
   const int P = a.C * (a.Hq / a.Hkv);
-  dim3 grid((P + BM - 1) / BM, a.Hkv, n_list);
+  const int nqt = (P + BM - 1) / BM;
+  dim3 grid(nqt * a.Hkv * n_list);
   if (head_dim == 64) {
-    hipLaunchKernelGGL(attn_fwd<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_fwd<64>, grid, dim3(256), 0, s, a, nqt);
   } else {
-    hipLaunchKernelGGL(attn_fwd<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_fwd<128>, grid, dim3(256), 0, s, a, nqt);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_dim,
                          hipStream_t s) {
-  dim3 grid((max_T + BK - 1) / BK, a.Hkv, n_list);
+  const int nkb = (max_T + BK - 1) / BK;
+  dim3 grid(nkb * a.Hkv * n_list);
   if (head_dim == 64) {
-    hipLaunchKernelGGL(attn_colsum<64>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_colsum<64>, grid, dim3(256), 0, s, a, nkb);
   } else {
-    hipLaunchKernelGGL(attn_colsum<128>, grid, dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attn_colsum<128>, grid, dim3(256), 0, s, a, nkb);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
