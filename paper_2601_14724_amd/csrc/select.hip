@@ -66,6 +66,22 @@ __device__ double block_sum_f64(double v, double *sh) {
   return t;
 }
 
+// hist[d] += 1 for every active lane with d >= 0.  Lanes holding the same
+// digit are merged with a ballot first (the leading digits of fp32 keys are
+// shared by most candidates, so plain LDS atomics would serialise).
+__device__ __forceinline__ void hist_add(unsigned *hist, int d) {
+  const int lane = threadIdx.x & 63;
+  unsigned long long active = __ballot(d >= 0);
+  for (int it = 0; it < 3 && active != 0ull; ++it) {
+    const int leader = __ffsll(active) - 1;
+    const int dl = __shfl(d, leader);
+    const unsigned long long m = __ballot(d == dl);
+    if (lane == leader) atomicAdd(&hist[dl], (unsigned)__popcll(m));
+    active &= ~m;
+  }
+  if ((active >> lane) & 1ull) atomicAdd(&hist[d], 1u);
+}
+
 struct SelectShared {
   unsigned hist[256];
   int digit, above;
@@ -75,8 +91,9 @@ struct SelectShared {
 
 // Keep the M largest of keys[0..T) (M < T), ties to the higher index; write
 // the kept indices ascending to out (and out2 if non-null).
-__device__ void select_top(const uint32_t *keys, int T, int M, int32_t *out, int32_t *out2,
-                           SelectShared &sh) {
+template <typename KeyPtr>
+__device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *out, int32_t *out2,
+                                           SelectShared &sh) {
   const int tid = threadIdx.x;
   uint32_t prefix = 0u, pmask = 0u;
   int want = M;
@@ -90,7 +107,7 @@ __device__ void select_top(const uint32_t *keys, int T, int M, int32_t *out, int
     __syncthreads();
     for (int i = tid; i < T; i += NT) {
       const uint32_t k = keys[i];
-      if ((k & pmask) == prefix) atomicAdd(&sh.hist[(k >> shift) & 255u], 1u);
+      hist_add(sh.hist, (k & pmask) == prefix ? (int)((k >> shift) & 255u) : -1);
     }
     __syncthreads();
     if (tid < 64) {
@@ -165,8 +182,27 @@ __device__ __forceinline__ double class_score(int cls, double om, double a, doub
   return (1.0 - om) * a + om * r;
 }
 
+// Candidates whose positions / keys fit in LDS take the LDS path; longer
+// layers fall back to global memory (L2-resident) with the same arithmetic.
+constexpr int kLdsKeys = 38400;   // 150 KiB
+
+// Index of `target` in the sorted array p[0..n), or -1.
+template <typename Ptr>
+__device__ __forceinline__ int find_sorted(Ptr p, int n, int target, int hint) {
+  if (hint < n && p[hint] == target) return hint;   // same physical index
+  int lo = 0, hi = n - 1;
+  while (lo <= hi) {
+    const int mid = (lo + hi) >> 1;
+    const int v = p[mid];
+    if (v == target) return mid;
+    if (v < target) lo = mid + 1; else hi = mid - 1;
+  }
+  return -1;
+}
+
 __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
   __shared__ SelectShared sh;
+  __shared__ uint32_t big[kLdsKeys];
   const int tid = threadIdx.x;
   const int l = a.layer_id[blockIdx.x];
   const LayerTable &L0 = a.tab[l];
@@ -197,59 +233,83 @@ __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
   const bool needA0 = cls != HERMES_SHALLOW, needR0 = cls != HERMES_DEEP;
   const bool needA1 = has_next && cls1 != HERMES_SHALLOW;
   const bool needR1 = has_next && cls1 != HERMES_DEEP;
+  const bool lds = T <= kLdsKeys && T1 <= kLdsKeys;
+  const bool by_pos = has_next && a.align_mode == 0;
 
-  // Normalisers: sum of alpha-weighted mass, sum of the recency curve.
-  double sa0 = 0.0, sa1 = 0.0, z0 = 0.0, z1 = 0.0;
-  for (int i = tid; i < T; i += NT) {
-    if (needA0) sa0 += mass_over_observers(w[i], i, T0, C, a.alpha_mode);
-    if (needR0) z0 += exp(-k * (double)(T - 1 - i));
-  }
-  for (int i = tid; i < T1; i += NT) {
-    if (needA1) sa1 += mass_over_observers(w1[i], i, T01, C, a.alpha_mode);
-    if (needR1) z1 += exp(-k * (double)(T1 - 1 - i));
-  }
+  // Normalisers: the alpha-weighted mass summed in a fixed order, and the
+  // recency curve's closed-form sum Z = (1 - e^{-kT}) / (1 - e^{-k}).
+  double sa0 = 0.0, sa1 = 0.0;
+  if (needA0)
+    for (int i = tid; i < T; i += NT) sa0 += mass_over_observers(w[i], i, T0, C, a.alpha_mode);
+  if (needA1)
+    for (int i = tid; i < T1; i += NT) sa1 += mass_over_observers(w1[i], i, T01, C, a.alpha_mode);
+  if (lds && by_pos)
+    for (int i = tid; i < T1; i += NT) big[i] = (uint32_t)pos1[i];
   sa0 = block_sum_f64(sa0, sh.red);
-  z0 = block_sum_f64(z0, sh.red);
   sa1 = block_sum_f64(sa1, sh.red);
-  z1 = block_sum_f64(z1, sh.red);
+  const double z0 = expm1(-k * (double)T) / expm1(-k);
+  const double z1 = expm1(-k * (double)T1) / expm1(-k);
 
   uint32_t *keys = a.keys + l * a.keys_lstride;
-  for (int i = tid; i < T; i += NT) {
-    const double a_i = needA0 ? mass_over_observers(w[i], i, T0, C, a.alpha_mode) / sa0 : 0.0;
-    const double r_i = needR0 ? exp(-k * (double)(T - 1 - i)) / z0 : 0.0;
-    double st = class_score(cls, om, a_i, r_i);
-    if (has_next) {
-      int jx = -1;
-      if (a.align_mode == 0) {
-        const int target = pos[i];
-        int lo = 0, hi = T1 - 1;
-        while (lo <= hi) {
-          const int mid = (lo + hi) >> 1;
-          const int v = pos1[mid];
-          if (v == target) {
-            jx = mid;
-            break;
-          }
-          if (v < target) lo = mid + 1; else hi = mid - 1;
-        }
-      } else if (i < T1) {
-        jx = i;
-      }
-      double s1 = 0.0;
-      if (jx >= 0) {
-        const double a_j = needA1 ? mass_over_observers(w1[jx], jx, T01, C, a.alpha_mode) / sa1 : 0.0;
-        const double r_j = needR1 ? exp(-k * (double)(T1 - 1 - jx)) / z1 : 0.0;
-        s1 = class_score(cls1, om1, a_j, r_j);
-      }
-      st = (1.0 - lam) * st + lam * s1;
+  const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
+  const double inv_z0 = 1.0 / z0, inv_z1 = T1 > 0 ? 1.0 / z1 : 0.0;
+  constexpr int U = 4;   // candidates per thread per pass: their loads are in flight together
+  for (int i0 = tid; i0 < T; i0 += U * NT) {
+    int ii[U], pv[U], jx[U];
+    float wv[U], w1v[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      ii[u] = i0 + u * NT;
+      const bool ok = ii[u] < T;
+      wv[u] = (ok && needA0) ? w[ii[u]] : 0.f;
+      pv[u] = (ok && by_pos) ? pos[ii[u]] : 0;
     }
-    const float f = (float)st;
-    keys[i] = __builtin_bit_cast(uint32_t, f);
-    if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      jx[u] = -1;
+      if (ii[u] < T && has_next) {
+        if (by_pos) {
+          jx[u] = lds ? find_sorted(reinterpret_cast<const int32_t *>(big), T1, pv[u], ii[u])
+                      : find_sorted(pos1, T1, pv[u], ii[u]);
+        } else {
+          jx[u] = ii[u] < T1 ? ii[u] : -1;
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < U; ++u) w1v[u] = (jx[u] >= 0 && needA1) ? w1[jx[u]] : 0.f;
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int i = ii[u];
+      if (i >= T) continue;
+      const double a_i = needA0 ? mass_over_observers(wv[u], i, T0, C, a.alpha_mode) * inv_sa0 : 0.0;
+      const double r_i = needR0 ? exp(-k * (double)(T - 1 - i)) * inv_z0 : 0.0;
+      double st = class_score(cls, om, a_i, r_i);
+      if (has_next) {
+        double s1 = 0.0;
+        const int j = jx[u];
+        if (j >= 0) {
+          const double a_j = needA1 ? mass_over_observers(w1v[u], j, T01, C, a.alpha_mode) * inv_sa1 : 0.0;
+          const double r_j = needR1 ? exp(-k * (double)(T1 - 1 - j)) * inv_z1 : 0.0;
+          s1 = class_score(cls1, om1, a_j, r_j);
+        }
+        st = (1.0 - lam) * st + lam * s1;
+      }
+      const float f = (float)st;
+      keys[i] = __builtin_bit_cast(uint32_t, f);
+      if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
+    }
   }
   __syncthreads();
   if (T <= L0.budget) return;
-  select_top(keys, T, L0.budget, a.kept + l * a.kept_lstride, L0.kept_dbg, sh);
+  int32_t *kept = a.kept + l * a.kept_lstride;
+  if (lds) {
+    for (int i = tid; i < T; i += NT) big[i] = keys[i];
+    __syncthreads();
+    select_top(big, T, L0.budget, kept, L0.kept_dbg, sh);
+  } else {
+    select_top(keys, T, L0.budget, kept, L0.kept_dbg, sh);
+  }
 }
 
 __global__ __launch_bounds__(NT) void topk_keys(const uint32_t *keys, int n, int k, int32_t *out) {
