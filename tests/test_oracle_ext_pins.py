@@ -1,0 +1,239 @@
+"""Pins of the extension oracle (summary token, re-indexing, guidance-prompt
+scoring, layer-weighted budgets) against facts that do not come from the
+oracle itself: the input generator's independent RoPE, closed forms, exact
+integer arithmetic written out here, and invariants."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+
+from oracle import hermes_extensions as he
+from oracle import hermes_oracle as ho
+from paper_2601_14724_amd import workloads as wk
+
+RNG = np.random.default_rng(20260114)
+
+
+def _raw(n, h=2, d=16):
+    return RNG.standard_normal((n, h, d))
+
+
+# ---------------------------------------------------------------- rounding
+
+def test_round_to_bf16_matches_generator_rounding():
+    x = RNG.standard_normal(4096).astype(np.float32).astype(np.float64) * 3.0
+    ours = he.round_to_bf16(x)
+    gen = wk.bf16_bits_to_f64(wk.f32_to_bf16_bits(x.astype(np.float32)))
+    assert np.array_equal(ours, gen)
+
+
+def test_round_to_bf16_ties_to_even():
+    # 1 + 2^-8 lies halfway between 1 and 1 + 2^-7: ties go to the even 1.0;
+    # 1 + 3 * 2^-8 lies halfway between 1 + 2^-7 and 1 + 2^-6: goes to 1 + 2^-6
+    assert he.round_to_bf16(np.array([1 + 2.0 ** -8]))[0] == 1.0
+    assert he.round_to_bf16(np.array([1 + 3 * 2.0 ** -8]))[0] == 1 + 2.0 ** -6
+
+
+# ---------------------------------------------------------------- RotaryDelta
+
+def test_rotary_delta_zero_is_identity():
+    k = _raw(5)
+    assert np.array_equal(he.rotary_delta(k, np.zeros(5, dtype=np.int64)), k)
+
+
+@pytest.mark.parametrize("d", [16, 64, 128])
+def test_rotary_delta_moves_rope_positions(d):
+    """Re-rotating a key made at p_old by p_new - p_old gives the key made at
+    p_new (the generator's RoPE is an independent implementation)."""
+    x = _raw(7, 3, d)
+    p_old = np.array([0, 5, 17, 300, 9000, 20000, 35903])
+    p_new = np.array([3, 4, 5, 6, 7, 8, 36000])
+    k_old = wk.rope_f64(x, p_old)
+    got = he.rotary_delta(k_old, p_new - p_old)
+    want = wk.rope_f64(x, p_new)
+    assert np.max(np.abs(got - want)) < 1e-9
+
+
+def test_rotary_delta_composes_and_preserves_pair_norms():
+    k = _raw(6, 2, 32)
+    a = np.array([1, -4, 100, 7, 0, 12345])
+    b = np.array([9, 4, -50, 1000, 3, -12345])
+    assert np.max(np.abs(he.rotary_delta(he.rotary_delta(k, a), b) - he.rotary_delta(k, a + b))) < 1e-10
+    r = he.rotary_delta(k, a)
+    n0 = k[..., :16] ** 2 + k[..., 16:] ** 2
+    n1 = r[..., :16] ** 2 + r[..., 16:] ** 2
+    assert np.max(np.abs(n0 - n1)) < 1e-12
+
+
+# ---------------------------------------------------------------- summary token
+
+def test_summary_key_is_mean_raw_key_at_target():
+    """Keys made at positions p_i and aligned to t average to the key made at
+    t from the mean unrotated vector."""
+    x = _raw(11, 2, 64)
+    p = np.sort(RNG.choice(5000, size=11, replace=False))
+    k = wk.rope_f64(x, p)
+    v = _raw(11, 2, 64)
+    ks, vs, t = he.summary_token(k, v, p)
+    assert t == p.max()
+    want = wk.rope_f64(x.mean(axis=0)[None], np.array([t]))[0]
+    assert np.max(np.abs(ks - want)) < 1e-10
+    # V: rows a_i * u average to mean(a) * u
+    a = RNG.standard_normal(11)
+    u = _raw(1, 2, 64)[0]
+    _, vs2, _ = he.summary_token(k, a[:, None, None] * u[None], p)
+    assert np.max(np.abs(vs2 - a.mean() * u)) < 1e-12
+
+
+def test_summary_of_one_token_is_that_token():
+    k, v = _raw(1, 2, 32), _raw(1, 2, 32)
+    ks, vs, t = he.summary_token(k, v, np.array([77]))
+    assert t == 77 and np.array_equal(ks, k[0]) and np.array_equal(vs, v[0])
+
+
+# ---------------------------------------------------------------- re-indexing
+
+def test_reindex_positions_left_compacts_behind_prefix():
+    assert list(he.reindex_positions(np.array([5, 9, 100, 101]), 3)) == [3, 4, 5, 6]
+    assert list(he.reindex_positions(np.array([0, 1, 2]), 0)) == [0, 1, 2]
+
+
+def test_reindex_of_contiguous_positions_changes_nothing():
+    k = he.round_to_bf16(_raw(4, 2, 32))
+    rp = np.array([10, 11, 12, 13])
+    k_new, p_new = he.reindex_keys(k, rp, 10)
+    assert list(p_new) == [10, 11, 12, 13] and np.array_equal(k_new, k)
+
+
+def test_reindexed_keys_are_keys_made_at_new_positions():
+    x = _raw(5, 2, 64)
+    p_old = np.array([100, 2000, 2001, 30000, 35000])
+    k_new, p_new = he.reindex_keys(wk.rope_f64(x, p_old), p_old, 7)
+    assert list(p_new) == [7, 8, 9, 10, 11]
+    want = he.round_to_bf16(wk.rope_f64(x, p_new))
+    # both sides round fp64 values that agree to ~1e-12: at most one bf16 ulp apart
+    ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(want), 1e-30))) - 7)
+    assert np.all(np.abs(k_new - want) <= ulp)
+
+
+# ---------------------------------------------------------------- guidance scoring
+
+def test_guidance_mass_uniform_closed_form():
+    """Zero queries: prompt row r attends T + r + 1 keys uniformly, so each
+    cached token receives Hq * sum_r 1 / (T + r + 1)."""
+    T, n, Hq, Hkv, d = 37, 5, 4, 2, 16
+    kc, vc = _raw(T, Hkv, d), _raw(T, Hkv, d)
+    kg, vg = _raw(n, Hkv, d), _raw(n, Hkv, d)
+    w = he.guidance_mass(np.zeros((n, Hq, d)), kc, vc, kg, vg)
+    want = Hq * sum(1.0 / (T + r + 1) for r in range(n))
+    assert w.shape == (T,) and np.max(np.abs(w - want)) < 1e-13
+
+
+def test_guidance_mass_plus_self_mass_is_rows_times_heads():
+    T, n, Hq, Hkv, d = 50, 6, 4, 2, 16
+    q, kc, vc, kg, vg = _raw(n, Hq, d), _raw(T, Hkv, d), _raw(T, Hkv, d), _raw(n, Hkv, d), _raw(n, Hkv, d)
+    _, w_all = ho.chunk_attention(q, kc, vc, kg, vg)
+    w = he.guidance_mass(q, kc, vc, kg, vg)
+    assert np.array_equal(w, w_all[:T])
+    assert abs(w_all.sum() - n * Hq) < 1e-12
+    a = he.guidance_importance(w, n)
+    assert abs(a.sum() - 1.0) < 1e-14
+
+
+# ---------------------------------------------------------------- budgets
+
+def test_budget_allocation_paper_weights_by_hand():
+    """Weights 0.7 / 1.0 / 1.3 (shallow / middle / deep) over the 3/17/8
+    partition of 28 layers and |M| = 6000 * 28, in integer arithmetic:
+    floor(7 * 168000 / 295) = 3986, floor(10 * 168000 / 295) = 5694,
+    floor(13 * 168000 / 295) = 7403, residue 168000 - 167980 = 20."""
+    cls = ho.layer_partition(28)
+    w = [{ho.SHALLOW: 0.7, ho.MIDDLE: 1.0, ho.DEEP: 1.3}[c] for c in cls]
+    m = he.budget_allocation(w, 6000 * 28)
+    assert m[:3] == [3986] * 3 and m[3:20] == [5694] * 17 and m[20:27] == [7403] * 7
+    assert m[27] == 7403 + 20 and sum(m) == 168000
+
+
+@pytest.mark.parametrize("wts", [("1.0", "1.0", "1.0"), ("1.3", "1.0", "0.7"),
+                                 ("0.7", "1.6", "0.7"), ("0.7", "1.0", "1.3")])
+def test_budget_allocation_fp64_equals_exact(wts):
+    cls = ho.layer_partition(28)
+    ws = [wts[c] for c in cls]
+    m = he.budget_allocation([float(x) for x in ws], 6000 * 28)
+    assert m == he.budget_allocation_exact(ws, 6000 * 28)
+    assert sum(m) == 6000 * 28
+
+
+def test_budget_allocation_equal_weights():
+    m = he.budget_allocation([1.0] * 5, 103)
+    assert m == [20, 20, 20, 20, 23]
+
+
+# ---------------------------------------------------------------- the extended step
+
+def _tiny(L=4, T0=40, C=12, Hq=4, Hkv=2, d=16, budgets=(30, 30, 30, 30), seed=3):
+    rng = np.random.default_rng(seed)
+    r = lambda *s: he.round_to_bf16(rng.standard_normal(s) * 0.5)
+    caches = [he.ExtLayerCache(r(T0, Hkv, d), r(T0, Hkv, d), np.arange(T0), np.arange(T0)) for _ in range(L)]
+    chunks = [{"q": r(C, Hq, d), "k": r(C, Hkv, d), "v": r(C, Hkv, d), "pos": np.arange(T0, T0 + C)}
+              for _ in range(L)]
+    cfg = ho.OracleConfig(budgets=list(budgets), classes=[ho.SHALLOW, ho.MIDDLE, ho.DEEP, ho.DEEP])
+    return caches, chunks, cfg
+
+
+def test_ext_step_without_extensions_equals_step():
+    caches, chunks, cfg = _tiny()
+    a = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig())
+    b = ho.stream_step([ho.LayerCache(c.k, c.v, c.pos) for c in caches], chunks, cfg)
+    for l in range(4):
+        assert np.array_equal(a["kept"][l], b["kept"][l])
+        assert np.array_equal(a["caches"][l].k, b["caches"][l].k)
+        assert np.array_equal(a["caches"][l].pos, b["caches"][l].pos)
+
+
+def test_ext_step_summary_tokens():
+    caches, chunks, cfg = _tiny()
+    res = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(summary=True))
+    for l in range(4):
+        c, kept = res["caches"][l], res["kept"][l]
+        s = res["summaries"][l]
+        if cfg.classes[l] != ho.DEEP:
+            assert s is None and len(c.pos) == 30
+            continue
+        assert len(c.pos) == 31                      # |M| kept + the summary
+        ev = np.setdiff1d(np.arange(52), kept)
+        assert np.array_equal(s["evicted"], ev) and s["source"] == ev[-1]
+        assert c.pos[s["index"]] == res["appended"][l].pos[ev[-1]]
+        assert np.all(np.diff(c.pos) > 0) and np.all(np.diff(c.rpos) > 0)
+        assert np.array_equal(np.delete(c.pos, s["index"]), res["appended"][l].pos[kept])
+
+
+def test_ext_step_eager_and_lazy_reindex():
+    caches, chunks, cfg = _tiny()
+    eager = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(summary=True, reindex_mode=he.REINDEX_EAGER,
+                                                                 rope_offset=5))
+    assert eager["reindexed"]
+    for c in eager["caches"]:
+        assert list(c.rpos) == list(range(5, 5 + len(c.rpos)))
+    # largest retained position is 51; the lazy rule fires at 51 + 12 >= limit
+    lazy_no = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(reindex_mode=he.REINDEX_LAZY,
+                                                                   rope_limit=64, rope_headroom=12))
+    lazy_yes = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(reindex_mode=he.REINDEX_LAZY,
+                                                                    rope_limit=63, rope_headroom=12))
+    assert not lazy_no["reindexed"] and lazy_yes["reindexed"]
+    plain = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig())
+    for l in range(4):
+        assert np.array_equal(lazy_no["caches"][l].k, plain["caches"][l].k)
+        assert list(lazy_yes["caches"][l].rpos) == list(range(len(lazy_yes["caches"][l].rpos)))
+
+
+def test_ext_step_guidance_zero_queries_keep_newest_in_deep_layers():
+    """A zero-query prompt spreads its mass evenly over the cache, so deep-layer
+    scores tie and the tie rule keeps the newest |M| tokens (lambda = 0)."""
+    caches, chunks, cfg = _tiny()
+    cfg.lambdas = [0.0] * 4
+    prompts = [{"q": np.zeros((3, 4, 16)), "k": np.zeros((3, 2, 16)), "v": np.zeros((3, 2, 16))}] * 4
+    res = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(scoring_mode=he.SCORE_GUIDANCE), prompts)
+    for l in (2, 3):
+        assert np.allclose(res["w"][l], res["w"][l][0], rtol=1e-14)
+        assert list(res["kept"][l]) == list(range(22, 52))
