@@ -99,7 +99,25 @@ typedef struct {
   int32_t alpha_mode;
   int32_t align_mode;
   int32_t force_scores;
+  /* Adjacent parts of the method; all zero = the core streaming step.  */
+  int32_t summary_mode;    /* 1: every deep layer that evicts appends one summary
+                              token (see hermes_compress); needs rpos buffers     */
+  int32_t reindex_mode;    /* HERMES_REINDEX_*: position re-indexing at compress;
+                              needs rpos buffers                                  */
+  int32_t rope_offset;     /* length of the fixed system prefix: re-indexed
+                              entries take positions offset, offset + 1, ...      */
+  int32_t rope_limit;      /* lazy re-indexing: the model's position limit        */
+  int32_t rope_headroom;   /* lazy re-indexing fires when the largest retained
+                              RoPE position of any layer + headroom >= limit      */
+  double rope_theta;       /* RoPE base; <= 0 selects 1e6                          */
+  int32_t scoring_mode;    /* HERMES_SCORE_*: source of the attention mass W      */
 } hermes_config;
+
+/* Position re-indexing (Sec. 3.3; appendix, 1D RoPE re-indexing). */
+enum { HERMES_REINDEX_NONE = 0, HERMES_REINDEX_EAGER = 1, HERMES_REINDEX_LAZY = 2 };
+/* Source of W: the chunk's own queries (default) or a guidance prompt used as
+ * a pseudo-query (Sec. 3.1 deep-layer paragraph; appendix guidance prompts). */
+enum { HERMES_SCORE_CHUNK = 0, HERMES_SCORE_GUIDANCE = 1 };
 
 /*
  * Caller-owned device memory for ONE layer.
@@ -113,7 +131,12 @@ typedef struct {
  *  s_dbg        fp32 [cap] or NULL: smoothed selection keys S~ (parity).
  *  kept_dbg     int32 [budget] or NULL: kept indices of the last compaction.
  *  cap          rows per buffer; must be >= max(init_len, budget) + the
- *               largest chunk ever appended.
+ *               largest chunk ever appended (budget + 1 in deep layers when
+ *               summary_mode is on).
+ *  rpos[2]      int32 [cap] RoPE positions the stored keys were rotated with,
+ *               one per buffer, strictly increasing along the cache; buffer 0
+ *               holds the initial `init_len` values.  Required (non-NULL) when
+ *               summary_mode or reindex_mode is on, else ignored (may be NULL).
  */
 typedef struct {
   void *k[2];
@@ -124,6 +147,7 @@ typedef struct {
   int32_t *kept_dbg;
   int32_t cap;
   int32_t init_len;
+  int32_t *rpos[2];
 } hermes_layer_buffers;
 
 /* Bytes of device workspace hermes_kv_init needs for `cfg` (0 on a bad cfg). */
@@ -158,6 +182,34 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
                         void *stream);
 
 /*
+ * hermes_append_chunk for callers that rotate the chunk's Q/K at RoPE
+ * positions other than its stream positions (after re-indexing, Sec. 3.3):
+ * rope_pos is device int32 [n_new], the positions the chunk's keys carry,
+ * stored in rpos; NULL means rope_pos = pos.  They must exceed every RoPE
+ * position already in the layer.  Same errors as hermes_append_chunk.
+ */
+int hermes_append_chunk_at(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                           const void *v, const int32_t *pos, const int32_t *rope_pos,
+                           int32_t n_new, void *out, void *stream);
+
+/*
+ * Guidance-prompt scoring (scoring_mode HERMES_SCORE_GUIDANCE; Sec. 3.1
+ * deep-layer paragraph and the appendix guidance prompts): n_rows prompt
+ * tokens (q, k, v: device bf16, layout as hermes_append_chunk; stacked over
+ * layers for HERMES_ALL_LAYERS) are placed after every cached token of the
+ * layer; their causal attention over [cache; prompt] gives w[i] for the
+ * cached candidates i < len.  The prompt is not stored.  Call it after the
+ * step's append and before hermes_compress, for every layer whose score
+ * needs W (non-shallow layers; middle layers take the hybrid local + global
+ * prompt, deep layers the global one).  Every candidate is seen by all
+ * prompt rows, so A = W / sum W.
+ * Errors: EINVAL (null pointer, layer, n_rows < 1 or > max_chunk), ESTATE
+ * (scoring_mode is not guidance, layer not appended this step, poisoned), EHIP.
+ */
+int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                          const void *v, int32_t n_rows, void *stream);
+
+/*
  * Close the step: for every layer whose length T exceeds its budget, score
  * the candidates (Sec. 3.1), smooth with layer l+1 (Sec. 3.2), keep the
  * budget largest keys (ties to the newer token) and compact K, V and
@@ -165,6 +217,24 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
  * Layers within budget are untouched.  Lengths become min(T, budget) on the
  * host, without a device read-back.  Requires every layer to have been
  * appended this step (or none, which makes the call a no-op).
+ *
+ * summary_mode 1 (Sec. 3.2 last paragraph; appendix summary-token
+ * algorithm): each evicting deep layer folds its evicted tokens into one
+ * token, V = mean of the evicted values, K = mean of the evicted keys each
+ * rotated from its RoPE position to t, the RoPE position of the newest
+ * evicted token.  The summary takes that token's stream and RoPE position
+ * and its sorted place among the kept rows, in addition to the budget
+ * (length budget + 1).  K and V are accumulated in fp64, stored as bf16.
+ *
+ * reindex_mode (Sec. 3.3; appendix 1D re-indexing): EAGER re-indexes every
+ * layer at every call, LAZY only when the largest retained RoPE position of
+ * any layer + rope_headroom >= rope_limit (decided on the device).  Entry j
+ * of a re-indexed layer gets RoPE position rope_offset + j and its key is
+ * rotated by the position change (rotate-half pairs, angles and rotation in
+ * fp64, stored as bf16); V is unchanged.
+ *
+ * scoring_mode GUIDANCE: W must have been written by hermes_guidance_score
+ * this step for every layer whose decision needs it, else ESTATE.
  * Errors: ESTATE, EHIP.
  */
 int hermes_compress(hermes_ctx *ctx, void *stream);
@@ -192,6 +262,21 @@ int hermes_kv_rewind(hermes_ctx *ctx);
 int hermes_kv_view(const hermes_ctx *ctx, int32_t layer, const void **k, const void **v,
                    const int32_t **pos, int32_t *len);
 
+/* Current RoPE-position buffer of one layer (NULL when the context keeps
+ * none); it has the length hermes_kv_view reports. */
+int hermes_kv_view_rope(const hermes_ctx *ctx, int32_t layer, const int32_t **rpos);
+
+/*
+ * Layer-dependent budgets from layer weights (Sec. 4 ablation "Layer-
+ * dependent Memory Budget"): budget[i] = floor((w[i] / sum_j w[j]) * total),
+ * evaluated in double with the sum taken in layer order, and the rounding
+ * residue added to the last layer so the budgets sum to `total`.  Host only.
+ * Errors: EINVAL (null pointer, n_layers < 1, a weight not finite or < 0,
+ * all weights 0, total < n_layers, a resulting budget < 1).
+ */
+int hermes_budget_from_weights(const double *weights, int32_t n_layers, int64_t total,
+                               int32_t *budget);
+
 /* Free the host context (device buffers stay with the caller). */
 void hermes_kv_destroy(hermes_ctx *ctx);
 
@@ -211,12 +296,13 @@ int hermes_select_topk(const float *keys, int32_t n, int32_t k, int32_t *out_idx
 /*
  * Kernel timing with HIP events recorded on the launch stream around every
  * launch of one kernel class while enabled.  Kernel ids: 0 append copy,
- * 1 chunk attention, 2 attention-mass sweep, 3 score+select, 4 gather,
- * 5 query attention.  hermes_profile_read waits for the recorded events and
+ * 1 chunk attention, 2 attention-mass sweep, 3 score+select, 4 gather (and
+ * re-indexing), 5 query attention, 6 summary reduction, 7 guidance scoring.  hermes_profile_read waits for the recorded events and
  * returns the summed milliseconds and the launch count since the last read.
  */
 enum { HERMES_K_APPEND = 0, HERMES_K_ATTN = 1, HERMES_K_COLSUM = 2, HERMES_K_SELECT = 3,
-       HERMES_K_GATHER = 4, HERMES_K_QUERY = 5, HERMES_K_COUNT = 6 };
+       HERMES_K_GATHER = 4, HERMES_K_QUERY = 5, HERMES_K_SUMMARY = 6, HERMES_K_GUIDE = 7,
+       HERMES_K_COUNT = 8 };
 int hermes_profile_enable(hermes_ctx *ctx, int on);
 int hermes_profile_read(hermes_ctx *ctx, int kernel_id, double *ms_total, int64_t *count);
 

@@ -246,37 +246,52 @@ def stream_step_ext(caches: List[ExtLayerCache], chunks: List[dict], cfg: ho.Ora
         st = ho.smooth(scores[l], scores[l + 1] if nxt else None, cats[l].pos,
                        cats[l + 1].pos if nxt else None, cfg.lambdas[l], cfg.align_mode)
         smoothed.append(st)
-        cat = cats[l]
-        T = cat.k.shape[0]
         idx = ho.topk_indices(st, cfg.budgets[l])
         kept.append(idx)
-        k, v, pos, rpos = cat.k[idx], cat.v[idx], cat.pos[idx], cat.rpos[idx]
-        summ = None
-        if ext.summary and cfg.classes[l] == ho.DEEP and T > cfg.budgets[l]:
-            mask = np.ones(T, dtype=bool)
-            mask[idx] = False
-            ev = np.nonzero(mask)[0]
-            ks, vs, t = summary_token(cat.k[ev], cat.v[ev], cat.rpos[ev], ext.rope_theta)
-            newest = int(ev[-1])
-            ins = int(np.searchsorted(idx, newest))
-            k = np.insert(k, ins, round_to_bf16(ks), axis=0)
-            v = np.insert(v, ins, round_to_bf16(vs), axis=0)
-            pos = np.insert(pos, ins, cat.pos[newest])
-            rpos = np.insert(rpos, ins, t)
-            summ = {"index": ins, "source": newest, "t": t, "evicted": ev,
-                    "k": round_to_bf16(ks), "v": round_to_bf16(vs)}
+        c, summ = compact_layer(cats[l], idx, cfg.classes[l] == ho.DEEP, ext)
         summaries.append(summ)
-        compact.append(ExtLayerCache(k, v, pos, rpos))
+        compact.append(c)
+    compact, reindexed = reindex_layers(compact, ext)
+    return {"out": outs, "w": ws, "scores": scores, "smoothed": smoothed, "kept": kept,
+            "caches": compact, "appended": cats, "summaries": summaries, "reindexed": reindexed}
+
+
+def compact_layer(cat: ExtLayerCache, idx: np.ndarray, deep: bool, ext: ExtConfig):
+    """Gather the kept rows of one appended layer (Sec. 3.2) and, for an
+    evicting deep layer with summaries on, insert the summary token of the
+    evicted rows at the sorted place of the newest evicted token."""
+    T = cat.k.shape[0]
+    k, v, pos, rpos = cat.k[idx], cat.v[idx], cat.pos[idx], cat.rpos[idx]
+    summ = None
+    if ext.summary and deep and len(idx) < T:
+        mask = np.ones(T, dtype=bool)
+        mask[idx] = False
+        ev = np.nonzero(mask)[0]
+        ks, vs, t = summary_token(cat.k[ev], cat.v[ev], cat.rpos[ev], ext.rope_theta)
+        newest = int(ev[-1])
+        ins = int(np.searchsorted(idx, newest))
+        k = np.insert(k, ins, round_to_bf16(ks), axis=0)
+        v = np.insert(v, ins, round_to_bf16(vs), axis=0)
+        pos = np.insert(pos, ins, cat.pos[newest])
+        rpos = np.insert(rpos, ins, t)
+        summ = {"index": ins, "source": newest, "t": t, "evicted": ev,
+                "k": round_to_bf16(ks), "v": round_to_bf16(vs)}
+    return ExtLayerCache(k, v, pos, rpos), summ
+
+
+def reindex_layers(compact: List[ExtLayerCache], ext: ExtConfig):
+    """Eager: re-index every layer.  Lazy: re-index every layer when the
+    largest retained RoPE position of any layer + headroom reaches the limit."""
     reindexed = False
     if ext.reindex_mode == REINDEX_EAGER:
         reindexed = True
     elif ext.reindex_mode == REINDEX_LAZY:
         top = max(int(c.rpos[-1]) for c in compact if len(c.rpos))
         reindexed = top + ext.rope_headroom >= ext.rope_limit
-    if reindexed:
-        for l in range(L):
-            c = compact[l]
-            k_new, r_new = reindex_keys(c.k, c.rpos, ext.rope_offset, ext.rope_theta)
-            compact[l] = ExtLayerCache(k_new, c.v, c.pos, r_new)
-    return {"out": outs, "w": ws, "scores": scores, "smoothed": smoothed, "kept": kept,
-            "caches": compact, "appended": cats, "summaries": summaries, "reindexed": reindexed}
+    if not reindexed:
+        return compact, False
+    out = []
+    for c in compact:
+        k_new, r_new = reindex_keys(c.k, c.rpos, ext.rope_offset, ext.rope_theta)
+        out.append(ExtLayerCache(k_new, c.v, c.pos, r_new))
+    return out, True

@@ -91,7 +91,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   const uint16_t *q = a.q + slot * a.q_lstride;
   const uint16_t *kn = a.kn + slot * a.kv_lstride;
   const uint16_t *vn = a.vn + slot * a.kv_lstride;
-  uint16_t *out = a.out + slot * a.q_lstride;
+  uint16_t *out = a.out != nullptr ? a.out + slot * a.q_lstride : nullptr;
   const uint16_t *kc = lt.k[cur];
   const uint16_t *vc = lt.v[cur];
 
@@ -271,7 +271,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = 1.f / l_tot;
-  if (row_ok) {
+  if (row_ok && out != nullptr) {
     uint16_t *orow = out + ((int64_t)r * Hq + h) * D;
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
@@ -285,9 +285,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
         *reinterpret_cast<uint2 *>(orow + d0) = uint2{w0, w1};
       }
     }
-    if (a.lse != nullptr && half == 0) {
-      a.lse[layer * a.lse_lstride + (int64_t)kv * P + prow] = m_run + log2f(l_tot);
-    }
+  }
+  if (row_ok && a.lse != nullptr && half == 0) {
+    a.lse[layer * a.lse_lstride + (int64_t)kv * P + prow] = m_run + log2f(l_tot);
   }
 }
 
@@ -305,7 +305,7 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
   const int C = a.C, Hq = a.Hq, Hkv = a.Hkv;
   const int G = Hq / Hkv;
   const int P = C * G;
-  const int T = T0 + C;
+  const int T = a.ncand[j];        // candidates: T0 + C, or T0 for a prompt
   const int k0 = kblk * BK;
   if (k0 >= T) return;
 
@@ -481,7 +481,7 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
 __global__ __launch_bounds__(256) void mass_reduce(ColsumArgs a) {
   const int j = blockIdx.y;
   const int layer = a.layer_id[j];
-  const int T = a.T0[j] + a.C;
+  const int T = a.ncand[j];
   const int i = blockIdx.x * 256 + threadIdx.x;
   if (i >= T) return;
   const double *part = a.wpart + layer * a.wpart_lstride + i;

@@ -29,6 +29,7 @@ __global__ __launch_bounds__(NT) void append_rows(AppendArgs a) {
   }
   for (int e = blockIdx.x * NT + threadIdx.x; e < a.C; e += gridDim.x * NT) {
     L.pos[cur][T0 + e] = a.pos[e];
+    if (L.rpos[cur] != nullptr) L.rpos[cur][T0 + e] = a.rope_pos != nullptr ? a.rope_pos[e] : a.pos[e];
   }
 }
 
@@ -55,7 +56,10 @@ __global__ __launch_bounds__(NT) void gather_rows(GatherArgs a) {
     const uint4 vx = *reinterpret_cast<const uint4 *>(vs + so);
     *reinterpret_cast<uint4 *>(kd + dof) = kx;
     *reinterpret_cast<uint4 *>(vd + dof) = vx;
-    if (c == 0) L.pos[cur ^ 1][row] = L.pos[cur][src];
+    if (c == 0) {
+      L.pos[cur ^ 1][row] = L.pos[cur][src];
+      if (L.rpos[cur] != nullptr) L.rpos[cur ^ 1][row] = L.rpos[cur][src];
+    }
   }
 }
 

@@ -23,8 +23,8 @@ size_t round_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t tab, lse, keys, kept, wpart, total;
-  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride;
+  size_t tab, lse, keys, kept, wpart, spart, sumk, sumv, smeta, flag, total;
+  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride;
 };
 
 int max_budget(const hermes_config *c) {
@@ -56,6 +56,16 @@ int check_config(const hermes_config *c) {
   if (c->align_mode != 0 && c->align_mode != 1) return HERMES_EINVAL;
   if (!std::isfinite(c->omega0) || !std::isfinite(c->gamma)) return HERMES_EINVAL;
   if (!std::isfinite(c->forget_rate) || !std::isfinite(c->sm_scale)) return HERMES_EINVAL;
+  if (c->summary_mode != 0 && c->summary_mode != 1) return HERMES_EINVAL;
+  if (c->reindex_mode < HERMES_REINDEX_NONE || c->reindex_mode > HERMES_REINDEX_LAZY)
+    return HERMES_EINVAL;
+  if (c->scoring_mode != HERMES_SCORE_CHUNK && c->scoring_mode != HERMES_SCORE_GUIDANCE)
+    return HERMES_EINVAL;
+  if (c->rope_offset < 0 || c->rope_limit < 0 || c->rope_headroom < 0) return HERMES_EINVAL;
+  if (!std::isfinite(c->rope_theta)) return HERMES_EINVAL;
+  // The RoPE kernels give each lane one frequency and at most 8 rotate pairs.
+  if ((c->summary_mode || c->reindex_mode) && c->n_kv_heads * c->head_dim > 1024)
+    return HERMES_ENOTSUP;
   return HERMES_OK;
 }
 
@@ -76,6 +86,20 @@ Layout layout_of(const hermes_config *c) {
   s.wpart_lstride = (int64_t)c->n_kv_heads * c->max_cap;
   s.wpart = off;
   off = round_up(off + sizeof(double) * (size_t)s.wpart_lstride * c->n_layers);
+  // summary token: fp64 block sums, staged bf16 rows and their metadata
+  const int64_t row = (int64_t)c->n_kv_heads * c->head_dim;
+  const int64_t nblk = c->summary_mode ? (c->max_cap + kSummaryRows - 1) / kSummaryRows : 0;
+  s.spart_lstride = nblk * 2 * row;
+  s.spart = off;
+  off = round_up(off + sizeof(double) * (size_t)s.spart_lstride * c->n_layers);
+  s.sumk = off;
+  off = round_up(off + (c->summary_mode ? sizeof(uint16_t) * (size_t)row * c->n_layers : 0));
+  s.sumv = off;
+  off = round_up(off + (c->summary_mode ? sizeof(uint16_t) * (size_t)row * c->n_layers : 0));
+  s.smeta = off;
+  off = round_up(off + sizeof(int32_t) * 4 * (size_t)c->n_layers);
+  s.flag = off;
+  off = round_up(off + sizeof(int32_t) * 4);
   s.total = off;
   return s;
 }
@@ -102,6 +126,11 @@ struct hermes_ctx {
   int L, Hq, Hkv, D, max_chunk, max_cap;
   double forget_rate, sm_scale;
   int alpha_mode, align_mode, force_scores;
+  int summary_mode, reindex_mode, scoring_mode;
+  int rope_offset, rope_limit, rope_headroom;
+  double rope_theta;
+  bool keep_rpos = false;
+  std::vector<int32_t> guided;      // prompt rows of this step's guidance score (0 = none)
   std::vector<int32_t> budget;
   std::vector<int8_t> cls;
   std::vector<double> lambda, omega;
@@ -199,6 +228,17 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
     if (b.cap < 1 || b.init_len < 0) return HERMES_EINVAL;
     if (b.cap > cfg->max_cap || b.init_len > b.cap || cfg->budget[l] > b.cap)
       return HERMES_ECAPACITY;
+    if (cfg->summary_mode || cfg->reindex_mode) {
+      for (int p = 0; p < 2; ++p)
+        if (b.rpos[p] == nullptr || !aligned(b.rpos[p], 4)) return HERMES_EINVAL;
+    }
+  }
+  if (cfg->summary_mode) {
+    // an evicting deep layer holds budget + 1 rows after compression
+    const std::vector<int8_t> cls = cfg->layer_class
+        ? std::vector<int8_t>(cfg->layer_class, cfg->layer_class + L) : default_classes(L);
+    for (int l = 0; l < L; ++l)
+      if (cls[l] == HERMES_DEEP && cfg->budget[l] + 1 > layers[l].cap) return HERMES_ECAPACITY;
   }
 
   hermes_ctx *c = new (std::nothrow) hermes_ctx();
@@ -214,6 +254,15 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
   c->alpha_mode = cfg->alpha_mode;
   c->align_mode = cfg->align_mode;
   c->force_scores = cfg->force_scores != 0;
+  c->summary_mode = cfg->summary_mode;
+  c->reindex_mode = cfg->reindex_mode;
+  c->scoring_mode = cfg->scoring_mode;
+  c->rope_offset = cfg->rope_offset;
+  c->rope_limit = cfg->rope_limit;
+  c->rope_headroom = cfg->rope_headroom;
+  c->rope_theta = cfg->rope_theta > 0.0 ? cfg->rope_theta : 1.0e6;
+  c->keep_rpos = cfg->summary_mode != 0 || cfg->reindex_mode != 0;
+  c->guided.assign(L, 0);
   c->budget.assign(cfg->budget, cfg->budget + L);
   c->cls = cfg->layer_class ? std::vector<int8_t>(cfg->layer_class, cfg->layer_class + L)
                             : default_classes(L);
@@ -253,6 +302,7 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
       t.k[p] = static_cast<uint16_t *>(layers[l].k[p]);
       t.v[p] = static_cast<uint16_t *>(layers[l].v[p]);
       t.pos[p] = layers[l].pos[p];
+      t.rpos[p] = c->keep_rpos ? layers[l].rpos[p] : nullptr;
     }
     t.w = layers[l].w;
     t.s_dbg = layers[l].s_dbg;
@@ -295,6 +345,7 @@ int hermes_kv_rewind(hermes_ctx *ctx) {
     ctx->len[l] = ctx->init_len[l];
     ctx->cur[l] = 0;
     ctx->appended[l] = 0;
+    ctx->guided[l] = 0;
   }
   ctx->n_appended = 0;
   ctx->step_n_new = 0;
@@ -312,9 +363,38 @@ int hermes_kv_view(const hermes_ctx *ctx, int32_t layer, const void **k, const v
   return HERMES_OK;
 }
 
-int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
-                        const void *v, const int32_t *pos, int32_t n_new, void *out,
-                        void *stream) {
+int hermes_kv_view_rope(const hermes_ctx *ctx, int32_t layer, const int32_t **rpos) {
+  if (ctx == nullptr || layer < 0 || layer >= ctx->L || rpos == nullptr) return HERMES_EINVAL;
+  *rpos = ctx->keep_rpos ? ctx->bufs[layer].rpos[ctx->cur[layer]] : nullptr;
+  return HERMES_OK;
+}
+
+int hermes_budget_from_weights(const double *weights, int32_t n_layers, int64_t total,
+                               int32_t *budget) {
+  if (weights == nullptr || budget == nullptr || n_layers < 1 || total < n_layers)
+    return HERMES_EINVAL;
+  double sum = 0.0;
+  for (int l = 0; l < n_layers; ++l) {
+    if (!std::isfinite(weights[l]) || weights[l] < 0.0) return HERMES_EINVAL;
+    sum += weights[l];
+  }
+  if (!(sum > 0.0)) return HERMES_EINVAL;
+  std::vector<int64_t> m(n_layers);
+  int64_t acc = 0;
+  for (int l = 0; l < n_layers; ++l) {
+    m[l] = (int64_t)std::floor((weights[l] / sum) * (double)total);
+    acc += m[l];
+  }
+  m[n_layers - 1] += total - acc;
+  for (int l = 0; l < n_layers; ++l)
+    if (m[l] < 1 || m[l] > INT32_MAX) return HERMES_EINVAL;
+  for (int l = 0; l < n_layers; ++l) budget[l] = (int32_t)m[l];
+  return HERMES_OK;
+}
+
+static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                       const void *v, const int32_t *pos, const int32_t *rope_pos, int32_t n_new,
+                       void *out, void *stream) {
   if (ctx == nullptr) return HERMES_EINVAL;
   if (ctx->poisoned) return HERMES_ESTATE;
   const int L = ctx->L;
@@ -322,7 +402,7 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   if (q == nullptr || k == nullptr || v == nullptr || pos == nullptr || out == nullptr)
     return HERMES_EINVAL;
   if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16) || !aligned(out, 16) ||
-      !aligned(pos, 4))
+      !aligned(pos, 4) || !aligned(rope_pos, 4))
     return HERMES_EINVAL;
   if (n_new < 1 || n_new > ctx->max_chunk) return HERMES_EINVAL;
   std::vector<int> list;
@@ -343,6 +423,7 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   auto base_len = [&](int l) { return ctx->appended[l] ? ctx->len[l] - ctx->step_n_new : ctx->len[l]; };
   auto evicts = [&](int l) { return base_len(l) + n_new > ctx->budget[l]; };
   auto need_w = [&](int l) {
+    if (ctx->scoring_mode == HERMES_SCORE_GUIDANCE) return false;   // W comes from the prompt
     if (ctx->force_scores) return true;
     if (ctx->cls[l] == HERMES_SHALLOW) return false;
     return evicts(l) || (l > 0 && evicts(l - 1) && ctx->lambda[l - 1] != 0.0);
@@ -361,6 +442,7 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   ap.kn = static_cast<const uint16_t *>(k);
   ap.vn = static_cast<const uint16_t *>(v);
   ap.pos = pos;
+  ap.rope_pos = rope_pos;
   ap.kv_lstride = kv_ls;
   ap.row_elems = ctx->Hkv * ctx->D;
   ap.C = n_new;
@@ -410,6 +492,7 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
     ap.cur[j] = at.cur[j] = ctx->cur[l];
     if (need_w(l)) {
       cs.T0[n_cs] = ctx->len[l];
+      cs.ncand[n_cs] = ctx->len[l] + n_new;
       cs.layer_id[n_cs] = (int8_t)l;
       cs.slot[n_cs] = slot;
       cs.cur[n_cs] = ctx->cur[l];
@@ -435,12 +518,111 @@ int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   return HERMES_OK;
 }
 
+int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                        const void *v, const int32_t *pos, int32_t n_new, void *out,
+                        void *stream) {
+  return append_impl(ctx, layer, q, k, v, pos, nullptr, n_new, out, stream);
+}
+
+int hermes_append_chunk_at(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                           const void *v, const int32_t *pos, const int32_t *rope_pos,
+                           int32_t n_new, void *out, void *stream) {
+  return append_impl(ctx, layer, q, k, v, pos, rope_pos, n_new, out, stream);
+}
+
+int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                          const void *v, int32_t n_rows, void *stream) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  if (ctx->poisoned) return HERMES_ESTATE;
+  const int L = ctx->L;
+  if (layer != HERMES_ALL_LAYERS && (layer < 0 || layer >= L)) return HERMES_EINVAL;
+  if (q == nullptr || k == nullptr || v == nullptr) return HERMES_EINVAL;
+  if (!aligned(q, 16) || !aligned(k, 16) || !aligned(v, 16)) return HERMES_EINVAL;
+  if (n_rows < 1 || n_rows > ctx->max_chunk) return HERMES_EINVAL;
+  if (ctx->scoring_mode != HERMES_SCORE_GUIDANCE) return HERMES_ESTATE;
+  std::vector<int> list;
+  for (int l = 0; l < L; ++l)
+    if (layer == HERMES_ALL_LAYERS || l == layer) list.push_back(l);
+  for (int l : list)
+    if (!ctx->appended[l]) return HERMES_ESTATE;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int64_t q_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_rows * ctx->Hq * ctx->D : 0;
+  const int64_t kv_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_rows * ctx->Hkv * ctx->D : 0;
+  const float scale_log2 = (float)(ctx->sm_scale * kLog2e);
+
+  // The prompt follows the cache: its rows attend [cache; prompt] causally
+  // (row LSE only), then the mass of the cached candidates only.
+  AttnArgs at;
+  std::memset(&at, 0, sizeof(at));
+  at.tab = ctx->d_tab;
+  at.q = static_cast<const uint16_t *>(q);
+  at.kn = static_cast<const uint16_t *>(k);
+  at.vn = static_cast<const uint16_t *>(v);
+  at.out = nullptr;
+  at.lse = reinterpret_cast<float *>(ctx->ws + ctx->lay.lse);
+  at.q_lstride = q_ls;
+  at.kv_lstride = kv_ls;
+  at.lse_lstride = ctx->lay.lse_lstride;
+  at.Hq = ctx->Hq;
+  at.Hkv = ctx->Hkv;
+  at.C = n_rows;
+  at.scale_log2 = scale_log2;
+  ColsumArgs cs;
+  std::memset(&cs, 0, sizeof(cs));
+  cs.tab = ctx->d_tab;
+  cs.q = at.q;
+  cs.kn = at.kn;
+  cs.vn = at.vn;
+  cs.lse = at.lse;
+  cs.wpart = reinterpret_cast<double *>(ctx->ws + ctx->lay.wpart);
+  cs.wpart_lstride = ctx->lay.wpart_lstride;
+  cs.wpart_hstride = ctx->max_cap;
+  cs.q_lstride = q_ls;
+  cs.kv_lstride = kv_ls;
+  cs.lse_lstride = at.lse_lstride;
+  cs.Hq = ctx->Hq;
+  cs.Hkv = ctx->Hkv;
+  cs.C = n_rows;
+  cs.scale_log2 = scale_log2;
+  int max_T = 0;
+  for (size_t j = 0; j < list.size(); ++j) {
+    const int l = list[j];
+    const int8_t slot = (int8_t)(layer == HERMES_ALL_LAYERS ? l : 0);
+    at.T0[j] = cs.T0[j] = ctx->len[l];
+    cs.ncand[j] = ctx->len[l];
+    at.layer_id[j] = cs.layer_id[j] = (int8_t)l;
+    at.slot[j] = cs.slot[j] = slot;
+    at.cur[j] = cs.cur[j] = ctx->cur[l];
+    max_T = ctx->len[l] > max_T ? ctx->len[l] : max_T;
+  }
+  const int n = (int)list.size();
+  const int rc = ctx->run(HERMES_K_GUIDE, s, [&] {
+    hipError_t e = launch_attention(at, n, ctx->D, s);
+    if (e != hipSuccess) return e;
+    return launch_colsum(cs, n, max_T, ctx->D, s);
+  });
+  if (rc != HERMES_OK) return rc;
+  for (int l : list) ctx->guided[l] = n_rows;
+  return HERMES_OK;
+}
+
 int hermes_compress(hermes_ctx *ctx, void *stream) {
   if (ctx == nullptr) return HERMES_EINVAL;
   if (ctx->poisoned) return HERMES_ESTATE;
   if (ctx->n_appended == 0) return HERMES_OK;
   if (ctx->n_appended != ctx->L) return HERMES_ESTATE;
+  const int L = ctx->L;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  auto evicts = [&](int l) { return ctx->len[l] > ctx->budget[l]; };
+  if (ctx->scoring_mode == HERMES_SCORE_GUIDANCE) {
+    // every layer whose decision reads W must have its prompt mass
+    for (int l = 0; l < L; ++l) {
+      if (ctx->cls[l] == HERMES_SHALLOW) continue;
+      const bool need = ctx->force_scores || evicts(l) ||
+                        (l > 0 && evicts(l - 1) && ctx->lambda[l - 1] != 0.0);
+      if (need && ctx->guided[l] == 0) return HERMES_ESTATE;
+    }
+  }
 
   SelectArgs sa;
   std::memset(&sa, 0, sizeof(sa));
@@ -450,7 +632,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
   sa.keys_lstride = ctx->lay.keys_lstride;
   sa.kept_lstride = ctx->lay.kept_lstride;
   sa.forget_rate = ctx->forget_rate;
-  sa.n_layers = ctx->L;
+  sa.n_layers = L;
   sa.C = ctx->step_n_new;
   sa.alpha_mode = ctx->alpha_mode;
   sa.align_mode = ctx->align_mode;
@@ -460,32 +642,121 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
   ga.kept = sa.kept;
   ga.kept_lstride = sa.kept_lstride;
   ga.row_elems = ctx->Hkv * ctx->D;
-  int n = 0;
-  for (int l = 0; l < ctx->L; ++l) {
+  ga.head_dim = ctx->D;
+  SummaryArgs sm;
+  std::memset(&sm, 0, sizeof(sm));
+  std::vector<int8_t> has_sum(L, 0);
+  int n = 0, n_sum = 0, max_T_sum = 0;
+  for (int l = 0; l < L; ++l) {
     sa.len[l] = ctx->len[l];
     sa.cur[l] = ctx->cur[l];
-    if (ctx->len[l] > ctx->budget[l]) {
+    sa.guide_rows[l] = ctx->scoring_mode == HERMES_SCORE_GUIDANCE ? ctx->guided[l] : 0;
+    if (evicts(l)) {
+      has_sum[l] = ctx->summary_mode && ctx->cls[l] == HERMES_DEEP;
       sa.layer_id[n] = (int8_t)l;
       ga.layer_id[n] = (int8_t)l;
       ga.cur[n] = ctx->cur[l];
-      ga.row_start[n + 1] = ga.row_start[n] + ctx->budget[l];
+      ga.mode[n] = 0;
+      ga.has_sum[n] = has_sum[l];
+      ga.row_start[n + 1] = ga.row_start[n] + ctx->budget[l] + has_sum[l];
       ++n;
+      if (has_sum[l]) {
+        sm.layer_id[n_sum] = (int8_t)l;
+        sm.cur[n_sum] = ctx->cur[l];
+        sm.len[n_sum] = ctx->len[l];
+        sm.budget[n_sum] = ctx->budget[l];
+        max_T_sum = ctx->len[l] > max_T_sum ? ctx->len[l] : max_T_sum;
+        ++n_sum;
+      }
     }
   }
-  sa.n_list = ga.n_list = n;
-  if (n > 0) {
-    int rc = ctx->run(HERMES_K_SELECT, s, [&] { return launch_select(sa, s); });
-    if (rc != HERMES_OK) return rc;
-    rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_gather(ga, s); });
+  sa.n_list = n;
+  const int n_evict = n;
+  int rc = HERMES_OK;
+  if (n_evict > 0) {
+    rc = ctx->run(HERMES_K_SELECT, s, [&] { return launch_select(sa, s); });
     if (rc != HERMES_OK) return rc;
   }
-  for (int l = 0; l < ctx->L; ++l) {
-    if (ctx->len[l] > ctx->budget[l]) {
+  if (!ctx->keep_rpos) {
+    ga.n_list = n_evict;
+    if (n_evict > 0) {
+      rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_gather(ga, s); });
+      if (rc != HERMES_OK) return rc;
+    }
+  } else {
+    int32_t *meta = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.smeta);
+    int32_t *flag = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.flag);
+    if (n_sum > 0) {
+      sm.tab = ctx->d_tab;
+      sm.kept = sa.kept;
+      sm.kept_lstride = sa.kept_lstride;
+      sm.part = reinterpret_cast<double *>(ctx->ws + ctx->lay.spart);
+      sm.part_lstride = ctx->lay.spart_lstride;
+      sm.sum_k = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.sumk);
+      sm.sum_v = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.sumv);
+      sm.sum_meta = meta;
+      sm.row_elems = ga.row_elems;
+      sm.head_dim = ctx->D;
+      sm.n_list = n_sum;
+      sm.theta = ctx->rope_theta;
+      rc = ctx->run(HERMES_K_SUMMARY, s, [&] { return launch_summary(sm, max_T_sum, s); });
+      if (rc != HERMES_OK) return rc;
+    }
+    // layers that kept everything are re-indexed in place
+    if (ctx->reindex_mode != HERMES_REINDEX_NONE) {
+      for (int l = 0; l < L; ++l) {
+        if (evicts(l) || ctx->len[l] == 0) continue;
+        ga.layer_id[n] = (int8_t)l;
+        ga.cur[n] = ctx->cur[l];
+        ga.mode[n] = 1;
+        ga.has_sum[n] = 0;
+        ga.row_start[n + 1] = ga.row_start[n] + ctx->len[l];
+        ++n;
+      }
+    }
+    ga.n_list = n;
+    ga.reindex = ctx->reindex_mode == HERMES_REINDEX_EAGER ? 1
+               : ctx->reindex_mode == HERMES_REINDEX_LAZY ? 2 : 0;
+    ga.rope_offset = ctx->rope_offset;
+    ga.theta = ctx->rope_theta;
+    ga.flag = flag;
+    ga.sum_k = reinterpret_cast<const uint16_t *>(ctx->ws + ctx->lay.sumk);
+    ga.sum_v = reinterpret_cast<const uint16_t *>(ctx->ws + ctx->lay.sumv);
+    ga.sum_meta = meta;
+    if (ctx->reindex_mode == HERMES_REINDEX_LAZY) {
+      DecideArgs da;
+      std::memset(&da, 0, sizeof(da));
+      da.tab = ctx->d_tab;
+      da.kept = sa.kept;
+      da.kept_lstride = sa.kept_lstride;
+      da.sum_meta = meta;
+      da.flag = flag;
+      da.n_layers = L;
+      da.limit = ctx->rope_limit;
+      da.headroom = ctx->rope_headroom;
+      for (int l = 0; l < L; ++l) {
+        da.len[l] = ctx->len[l];
+        da.budget[l] = ctx->budget[l];
+        da.cur[l] = ctx->cur[l];
+        da.evicts[l] = evicts(l);
+        da.has_sum[l] = has_sum[l];
+      }
+      rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_decide(da, s); });
+      if (rc != HERMES_OK) return rc;
+    }
+    if (n > 0) {
+      rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_gather_rope(ga, s); });
+      if (rc != HERMES_OK) return rc;
+    }
+  }
+  for (int l = 0; l < L; ++l) {
+    if (evicts(l)) {
       if (ctx->cur[l] == 1) ctx->buf0_dirty[l] = 1;
       ctx->cur[l] ^= 1;
-      ctx->len[l] = ctx->budget[l];
+      ctx->len[l] = ctx->budget[l] + has_sum[l];
     }
     ctx->appended[l] = 0;
+    ctx->guided[l] = 0;
   }
   ctx->n_appended = 0;
   return HERMES_OK;

@@ -16,6 +16,7 @@ struct LayerTable {
   uint16_t *k[2];
   uint16_t *v[2];
   int32_t *pos[2];
+  int32_t *rpos[2];         // RoPE positions of the stored keys (null when not kept)
   float *w;
   float *s_dbg;
   int32_t *kept_dbg;
@@ -29,7 +30,8 @@ struct LayerTable {
 
 // Chunk (or query) attention: launch entry j covers layer layer_id[j], reads
 // cached rows [0, T0[j]) of buffer cur[j] and new rows from the stacked inputs
-// at slot j (stride *_lstride elements), writes out (and lse if non-null).
+// at slot j (stride *_lstride elements), writes out (if non-null) and lse (if
+// non-null).
 struct AttnArgs {
   const LayerTable *tab;
   const uint16_t *q, *kn, *vn;
@@ -44,9 +46,11 @@ struct AttnArgs {
   int8_t cur[kMaxLayers];
 };
 
-// Attention-mass sweep: W_i for every candidate of layer layer_id[j].  Each
-// KV head's share goes to wpart[layer][kv][i] (fp64), then is summed into
-// the layer's w buffer in head order.
+// Attention-mass sweep: W_i for the candidates i < ncand[j] of layer
+// layer_id[j] (ncand = T0 + C for the chunk's own mass, T0 for a guidance
+// prompt, whose rows are not candidates).  Each KV head's share goes to
+// wpart[layer][kv][i] (fp64), then is summed into the layer's w buffer in
+// head order.
 struct ColsumArgs {
   const LayerTable *tab;
   const uint16_t *q, *kn, *vn;
@@ -56,6 +60,7 @@ struct ColsumArgs {
   int32_t Hq, Hkv, C;
   float scale_log2;
   int32_t T0[kMaxLayers];
+  int32_t ncand[kMaxLayers];
   int8_t layer_id[kMaxLayers];
   int8_t slot[kMaxLayers];
   int8_t cur[kMaxLayers];
@@ -72,20 +77,68 @@ struct SelectArgs {
   int32_t n_layers, C, alpha_mode, align_mode;
   int32_t n_list;
   int32_t len[kMaxLayers];
+  int32_t guide_rows[kMaxLayers];   // by layer: > 0 = W came from that many prompt rows
   int8_t cur[kMaxLayers];
   int8_t layer_id[kMaxLayers];
 };
 
-// Order-preserving gather of kept rows into the other buffer of each pair.
+// Order-preserving gather of kept rows into the other buffer of each pair,
+// optionally with a summary row inserted and with RoPE re-indexing.
+// mode[j] 0: rows [0, row_start[j+1] - row_start[j]) of the other buffer
+// from the kept list (and the summary row when has_sum[j]); mode 1: the
+// layer did not evict, re-index its current buffer in place.
 struct GatherArgs {
   const LayerTable *tab;
   const int32_t *kept;
   int64_t kept_lstride;
   int32_t row_elems;        // Hkv * d
+  int32_t head_dim;
   int32_t n_list;
-  int32_t row_start[kMaxLayers + 1];   // prefix of kept rows over the list
+  int32_t reindex;          // 0 never, 1 always, 2 when *flag != 0
+  int32_t rope_offset;
+  double theta;             // RoPE base
+  const int32_t *flag;      // lazy re-indexing decision (device)
+  const uint16_t *sum_k, *sum_v;   // [n_layers][row_elems] staged summary rows
+  const int32_t *sum_meta;  // [n_layers][4]: insert index, stream pos, RoPE pos, evicted
+  int32_t row_start[kMaxLayers + 1];   // prefix of output rows over the list
   int8_t layer_id[kMaxLayers];
   int8_t cur[kMaxLayers];
+  int8_t mode[kMaxLayers];
+  int8_t has_sum[kMaxLayers];
+};
+
+// Summary token of every listed (deep, evicting) layer: fp64 partial sums of
+// the evicted rows per block of kSummaryRows candidates, then the mean.
+struct SummaryArgs {
+  const LayerTable *tab;
+  const int32_t *kept;
+  int64_t kept_lstride;
+  double *part;             // [n_layers][blocks][2 * row_elems]
+  int64_t part_lstride;
+  uint16_t *sum_k, *sum_v;  // [n_layers][row_elems]
+  int32_t *sum_meta;        // [n_layers][4]
+  int32_t row_elems, head_dim, n_list;
+  double theta;             // RoPE base
+  int32_t len[kMaxLayers];      // by entry: candidates T
+  int32_t budget[kMaxLayers];   // by entry: kept M
+  int8_t layer_id[kMaxLayers];
+  int8_t cur[kMaxLayers];
+};
+
+// Lazy re-indexing decision: the largest RoPE position each layer retains
+// after this compression, against limit - headroom.
+struct DecideArgs {
+  const LayerTable *tab;
+  const int32_t *kept;
+  int64_t kept_lstride;
+  const int32_t *sum_meta;
+  int32_t *flag;
+  int32_t n_layers, limit, headroom;
+  int32_t len[kMaxLayers];      // by layer: T before compression
+  int32_t budget[kMaxLayers];
+  int8_t cur[kMaxLayers];
+  int8_t evicts[kMaxLayers];
+  int8_t has_sum[kMaxLayers];
 };
 
 // Append copy: new K/V rows and positions into rows [T0, T0 + C) of the
@@ -94,6 +147,7 @@ struct AppendArgs {
   const LayerTable *tab;
   const uint16_t *kn, *vn;
   const int32_t *pos;
+  const int32_t *rope_pos;  // RoPE positions of the new rows (null: = pos)
   int64_t kv_lstride;
   int32_t row_elems, C, n_list;
   int32_t T0[kMaxLayers];
@@ -110,9 +164,13 @@ hipError_t launch_select(const SelectArgs &a, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, hipStream_t s);
 hipError_t launch_topk(const float *keys, int n, int k, int32_t *out, hipStream_t s);
+hipError_t launch_summary(const SummaryArgs &a, int max_T, hipStream_t s);
+hipError_t launch_decide(const DecideArgs &a, hipStream_t s);
+hipError_t launch_gather_rope(const GatherArgs &a, hipStream_t s);
 
 // Geometry shared by host sizing and kernels.
 constexpr int kAttnRowsPerBlock = 128;   // packed (row, head) pairs per workgroup
 constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the sweep
+constexpr int kSummaryRows = 512;        // candidates per workgroup of the summary sums
 
 }  // namespace hermes

@@ -230,6 +230,10 @@ __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
     cls1 = L1.cls;
     om1 = L1.omega;
   }
+  // W from a guidance prompt: every candidate has the same observers, so the
+  // normalised mass is W / sum W whatever alpha_mode says.
+  const int am0 = a.guide_rows[l] > 0 ? 1 : a.alpha_mode;
+  const int am1 = (has_next && a.guide_rows[l + 1] > 0) ? 1 : a.alpha_mode;
   const bool needA0 = cls != HERMES_SHALLOW, needR0 = cls != HERMES_DEEP;
   const bool needA1 = has_next && cls1 != HERMES_SHALLOW;
   const bool needR1 = has_next && cls1 != HERMES_DEEP;
@@ -240,9 +244,9 @@ __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
   // recency curve's closed-form sum Z = (1 - e^{-kT}) / (1 - e^{-k}).
   double sa0 = 0.0, sa1 = 0.0;
   if (needA0)
-    for (int i = tid; i < T; i += NT) sa0 += mass_over_observers(w[i], i, T0, C, a.alpha_mode);
+    for (int i = tid; i < T; i += NT) sa0 += mass_over_observers(w[i], i, T0, C, am0);
   if (needA1)
-    for (int i = tid; i < T1; i += NT) sa1 += mass_over_observers(w1[i], i, T01, C, a.alpha_mode);
+    for (int i = tid; i < T1; i += NT) sa1 += mass_over_observers(w1[i], i, T01, C, am1);
   if (lds && by_pos)
     for (int i = tid; i < T1; i += NT) big[i] = (uint32_t)pos1[i];
   sa0 = block_sum_f64(sa0, sh.red);
@@ -282,14 +286,14 @@ __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
     for (int u = 0; u < U; ++u) {
       const int i = ii[u];
       if (i >= T) continue;
-      const double a_i = needA0 ? mass_over_observers(wv[u], i, T0, C, a.alpha_mode) * inv_sa0 : 0.0;
+      const double a_i = needA0 ? mass_over_observers(wv[u], i, T0, C, am0) * inv_sa0 : 0.0;
       const double r_i = needR0 ? exp(-k * (double)(T - 1 - i)) * inv_z0 : 0.0;
       double st = class_score(cls, om, a_i, r_i);
       if (has_next) {
         double s1 = 0.0;
         const int j = jx[u];
         if (j >= 0) {
-          const double a_j = needA1 ? mass_over_observers(w1v[u], j, T01, C, a.alpha_mode) * inv_sa1 : 0.0;
+          const double a_j = needA1 ? mass_over_observers(w1v[u], j, T01, C, am1) * inv_sa1 : 0.0;
           const double r_j = needR1 ? exp(-k * (double)(T1 - 1 - j)) * inv_z1 : 0.0;
           s1 = class_score(cls1, om1, a_j, r_j);
         }

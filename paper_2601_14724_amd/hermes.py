@@ -24,11 +24,15 @@ OK, EINVAL, ECAPACITY, ESTATE, EHIP, ENOTSUP = 0, -1, -2, -3, -4, -5
 SHALLOW, MIDDLE, DEEP = 0, 1, 2
 ALL_LAYERS = -1
 MAX_LAYERS = 64
-K_APPEND, K_ATTN, K_COLSUM, K_SELECT, K_GATHER, K_QUERY = range(6)
-KERNEL_NAMES = ("append", "attention", "colsum", "select", "gather", "query")
+K_APPEND, K_ATTN, K_COLSUM, K_SELECT, K_GATHER, K_QUERY, K_SUMMARY, K_GUIDE = range(8)
+KERNEL_NAMES = ("append", "attention", "colsum", "select", "gather", "query", "summary", "guide")
+REINDEX_NONE, REINDEX_EAGER, REINDEX_LAZY = 0, 1, 2
+SCORE_CHUNK, SCORE_GUIDANCE = 0, 1
 
-EXPORTED = ("hermes_workspace_bytes", "hermes_kv_init", "hermes_append_chunk", "hermes_compress",
-            "hermes_query_attend", "hermes_kv_rewind", "hermes_kv_view", "hermes_kv_destroy", "hermes_strerror",
+EXPORTED = ("hermes_workspace_bytes", "hermes_kv_init", "hermes_append_chunk",
+            "hermes_append_chunk_at", "hermes_guidance_score", "hermes_compress",
+            "hermes_query_attend", "hermes_kv_rewind", "hermes_kv_view", "hermes_kv_view_rope",
+            "hermes_budget_from_weights", "hermes_kv_destroy", "hermes_strerror",
             "hermes_select_topk", "hermes_profile_enable", "hermes_profile_read")
 
 
@@ -42,14 +46,19 @@ class HermesConfig(ctypes.Structure):
                 ("omega0", ctypes.c_double), ("gamma", ctypes.c_double),
                 ("forget_rate", ctypes.c_double), ("sm_scale", ctypes.c_double),
                 ("alpha_mode", ctypes.c_int32), ("align_mode", ctypes.c_int32),
-                ("force_scores", ctypes.c_int32)]
+                ("force_scores", ctypes.c_int32),
+                ("summary_mode", ctypes.c_int32), ("reindex_mode", ctypes.c_int32),
+                ("rope_offset", ctypes.c_int32), ("rope_limit", ctypes.c_int32),
+                ("rope_headroom", ctypes.c_int32), ("rope_theta", ctypes.c_double),
+                ("scoring_mode", ctypes.c_int32)]
 
 
 class LayerBuffers(ctypes.Structure):
     _fields_ = [("k", ctypes.c_void_p * 2), ("v", ctypes.c_void_p * 2),
                 ("pos", ctypes.c_void_p * 2), ("w", ctypes.c_void_p),
                 ("s_dbg", ctypes.c_void_p), ("kept_dbg", ctypes.c_void_p),
-                ("cap", ctypes.c_int32), ("init_len", ctypes.c_int32)]
+                ("cap", ctypes.c_int32), ("init_len", ctypes.c_int32),
+                ("rpos", ctypes.c_void_p * 2)]
 
 
 _vp, _i32, _i64, _dbl = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
@@ -60,6 +69,14 @@ lib.hermes_kv_init.argtypes = [ctypes.POINTER(HermesConfig), ctypes.POINTER(Laye
                                ctypes.c_size_t, ctypes.POINTER(_vp)]
 lib.hermes_append_chunk.restype = ctypes.c_int
 lib.hermes_append_chunk.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
+lib.hermes_append_chunk_at.restype = ctypes.c_int
+lib.hermes_append_chunk_at.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
+lib.hermes_guidance_score.restype = ctypes.c_int
+lib.hermes_guidance_score.argtypes = [_vp, _i32, _vp, _vp, _vp, _i32, _vp]
+lib.hermes_kv_view_rope.restype = ctypes.c_int
+lib.hermes_kv_view_rope.argtypes = [_vp, _i32, ctypes.POINTER(_vp)]
+lib.hermes_budget_from_weights.restype = ctypes.c_int
+lib.hermes_budget_from_weights.argtypes = [ctypes.POINTER(_dbl), _i32, _i64, ctypes.POINTER(_i32)]
 lib.hermes_compress.restype = ctypes.c_int
 lib.hermes_compress.argtypes = [_vp, _vp]
 lib.hermes_query_attend.restype = ctypes.c_int
@@ -108,6 +125,16 @@ def _need(t: torch.Tensor, dtype: torch.dtype, shape: tuple, name: str) -> None:
         raise ValueError(f"{name}: must be a contiguous device tensor")
 
 
+def budget_from_weights(weights: Sequence[float], total: int) -> list:
+    """Per-layer budgets floor(w_i / sum w * total), residue to the last layer
+    (the library's host helper)."""
+    n = len(weights)
+    w = (ctypes.c_double * n)(*[float(x) for x in weights])
+    out = (ctypes.c_int32 * n)()
+    check(lib.hermes_budget_from_weights(w, n, int(total), out), "hermes_budget_from_weights")
+    return list(out)
+
+
 def select_topk(keys: torch.Tensor, k: int) -> torch.Tensor:
     """Indices (ascending) of the k largest non-negative fp32 keys, ties to the
     higher index, computed by the library's TopK kernel."""
@@ -135,13 +162,17 @@ class HermesKV:
                  lambdas: Optional[Sequence[float]] = None, omega0: float = 0.75,
                  gamma: float = 0.6, forget_rate: float = 2.0 ** -10,
                  sm_scale: Optional[float] = None, alpha_mode: int = 0, align_mode: int = 0,
-                 force_scores: bool = False, debug: bool = False, device: str = "cuda"):
+                 force_scores: bool = False, debug: bool = False, device: str = "cuda",
+                 summary_mode: int = 0, reindex_mode: int = REINDEX_NONE, rope_offset: int = 0,
+                 rope_limit: int = 0, rope_headroom: int = 0, rope_theta: float = 1.0e6,
+                 scoring_mode: int = SCORE_CHUNK):
         self.L, self.Hq, self.Hkv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         self.budgets = [int(b) for b in budgets]
         self.max_chunk = int(max_chunk)
         init_lens = [0] * n_layers if init is None else [int(t[0].shape[0]) for t in init]
         if cap is None:
-            cap = max(max(init_lens), max(self.budgets)) + self.max_chunk
+            cap = max(max(init_lens), max(self.budgets) + int(bool(summary_mode))) + self.max_chunk
+        self.keep_rpos = bool(summary_mode) or reindex_mode != REINDEX_NONE
         self.cap = int(cap)
         self.device = torch.device(device)
         dev = self.device
@@ -152,17 +183,22 @@ class HermesKV:
                   for _ in range(n_layers)]
         self.pos = [[torch.zeros(self.cap, dtype=torch.int32, device=dev) for _ in range(2)]
                     for _ in range(n_layers)]
+        self.rpos = ([[torch.zeros(self.cap, dtype=torch.int32, device=dev) for _ in range(2)]
+                      for _ in range(n_layers)] if self.keep_rpos else None)
         self.w = [torch.zeros(self.cap, dtype=torch.float32, device=dev) for _ in range(n_layers)]
         self.s_dbg = ([torch.zeros(self.cap, dtype=torch.float32, device=dev)
                        for _ in range(n_layers)] if debug else None)
         self.kept_dbg = ([torch.zeros(b, dtype=torch.int32, device=dev) for b in self.budgets]
                          if debug else None)
         if init is not None:
-            for l, (k0, v0, p0) in enumerate(init):
+            for l, t in enumerate(init):
+                k0, v0, p0 = t[:3]
                 n = k0.shape[0]
                 self.k[l][0][:n].copy_(k0)
                 self.v[l][0][:n].copy_(v0)
                 self.pos[l][0][:n].copy_(p0)
+                if self.keep_rpos:    # RoPE positions (4th element), default the stream ones
+                    self.rpos[l][0][:n].copy_(t[3] if len(t) > 3 else p0)
         self._budget_arr = (ctypes.c_int32 * n_layers)(*self.budgets)
         self._class_arr = ((ctypes.c_int8 * n_layers)(*layer_class)
                            if layer_class is not None else None)
@@ -179,6 +215,9 @@ class HermesKV:
         cfg.omega0, cfg.gamma, cfg.forget_rate = omega0, gamma, forget_rate
         cfg.sm_scale = sm_scale if sm_scale is not None else 0.0
         cfg.alpha_mode, cfg.align_mode, cfg.force_scores = alpha_mode, align_mode, int(force_scores)
+        cfg.summary_mode, cfg.reindex_mode, cfg.scoring_mode = int(summary_mode), reindex_mode, scoring_mode
+        cfg.rope_offset, cfg.rope_limit, cfg.rope_headroom = rope_offset, rope_limit, rope_headroom
+        cfg.rope_theta = rope_theta
         self._cfg = cfg
         nbytes = lib.hermes_workspace_bytes(ctypes.byref(cfg))
         if nbytes == 0:
@@ -196,6 +235,9 @@ class HermesKV:
             b.kept_dbg = _ptr(self.kept_dbg[l]) if debug else None
             b.cap = self.cap
             b.init_len = init_lens[l]
+            if self.keep_rpos:
+                for p in range(2):
+                    b.rpos[p] = self.rpos[l][p].data_ptr()
         self._bufs = bufs
         ctx = ctypes.c_void_p()
         check(lib.hermes_kv_init(ctypes.byref(cfg), bufs, self.workspace.data_ptr(), nbytes,
@@ -210,16 +252,31 @@ class HermesKV:
         _need(v, torch.bfloat16, lead + (n, self.Hkv, self.d), "v")
 
     def append(self, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: torch.Tensor,
-               layer: int = ALL_LAYERS, out: Optional[torch.Tensor] = None) -> torch.Tensor:
+               layer: int = ALL_LAYERS, out: Optional[torch.Tensor] = None,
+               rope_pos: Optional[torch.Tensor] = None) -> torch.Tensor:
         n = q.shape[-3]
         self._check_inputs(q, k, v, n, layer)
         _need(pos, torch.int32, (n,), "pos")
         if out is None:
             out = torch.empty_like(q)
-        check(lib.hermes_append_chunk(self.ctx, layer, q.data_ptr(), k.data_ptr(), v.data_ptr(),
-                                      pos.data_ptr(), n, out.data_ptr(), _stream()),
-              "hermes_append_chunk")
+        if rope_pos is None:
+            check(lib.hermes_append_chunk(self.ctx, layer, q.data_ptr(), k.data_ptr(),
+                                          v.data_ptr(), pos.data_ptr(), n, out.data_ptr(),
+                                          _stream()), "hermes_append_chunk")
+        else:
+            _need(rope_pos, torch.int32, (n,), "rope_pos")
+            check(lib.hermes_append_chunk_at(self.ctx, layer, q.data_ptr(), k.data_ptr(),
+                                             v.data_ptr(), pos.data_ptr(), rope_pos.data_ptr(), n,
+                                             out.data_ptr(), _stream()), "hermes_append_chunk_at")
         return out
+
+    def guidance(self, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor,
+                 layer: int = ALL_LAYERS) -> None:
+        """Attention mass of the cached tokens from guidance-prompt rows."""
+        n = q.shape[-3]
+        self._check_inputs(q, k, v, n, layer)
+        check(lib.hermes_guidance_score(self.ctx, layer, q.data_ptr(), k.data_ptr(), v.data_ptr(),
+                                        n, _stream()), "hermes_guidance_score")
 
     def compress(self) -> None:
         check(lib.hermes_compress(self.ctx, _stream()), "hermes_compress")
@@ -251,6 +308,15 @@ class HermesKV:
         p = 0 if kp.value == self.k[layer][0].data_ptr() else 1
         n = ln.value
         return self.k[layer][p][:n], self.v[layer][p][:n], self.pos[layer][p][:n]
+
+    def view_rope(self, layer: int) -> torch.Tensor:
+        """RoPE positions of the layer's current buffer, first `len` rows."""
+        rp = ctypes.c_void_p()
+        check(lib.hermes_kv_view_rope(self.ctx, layer, ctypes.byref(rp)), "hermes_kv_view_rope")
+        if not rp.value:
+            raise ValueError("this cache keeps no RoPE positions")
+        p = 0 if rp.value == self.rpos[layer][0].data_ptr() else 1
+        return self.rpos[layer][p][:self.length(layer)]
 
     # -------------------------------------------------------------- profiling
     def profile(self, on: bool = True) -> None:

@@ -17,7 +17,8 @@ Generation recipe (per tensor):
   * rng = numpy default_rng(SeedSequence([workload_id, step, layer, tensor_id]))
     tensor ids: chunk Q=0, chunk K=1, chunk V=2, cache K=3, cache V=4,
     low-rank basis U=5, chunk low-rank coefficients=6, cache coefficients=7,
-    query Q=8, query K=9, query V=10;
+    query Q=8, query K=9, query V=10, guidance-prompt Q=11, K=12, V=13 (step
+    id 1000 for the global prompt, 1001 for the hybrid local + global one);
   * draw float64 N(0,1), scale by 0.5 (standard deviation 0.5);
   * the low-rank key workload adds 1.0 * (z @ U), U in R^{8 x d} with entries
     N(0, 1/8) per (layer, kv head) and z ~ N(0, I_8) per token, before scaling
@@ -44,6 +45,8 @@ T_CHUNK_Q, T_CHUNK_K, T_CHUNK_V = 0, 1, 2
 T_CACHE_K, T_CACHE_V = 3, 4
 T_LOWRANK_U, T_CHUNK_Z, T_CACHE_Z = 5, 6, 7
 T_QUERY_Q, T_QUERY_K, T_QUERY_V = 8, 9, 10
+T_PROMPT_Q, T_PROMPT_K, T_PROMPT_V = 11, 12, 13
+PROMPT_GLOBAL, PROMPT_HYBRID = 0, 1
 
 
 @dataclasses.dataclass(frozen=True)
@@ -188,6 +191,23 @@ def gen_query(wl: Workload, layer: int) -> dict:
     k = rope_f64(_gauss(_rng(wl, 0, layer, T_QUERY_K), (n, wl.n_kv_heads, wl.head_dim),
                         wl.scale), pos)
     v = _gauss(_rng(wl, 0, layer, T_QUERY_V), (n, wl.n_kv_heads, wl.head_dim), wl.scale)
+    return {"q": _to_bits(q), "k": _to_bits(k), "v": _to_bits(v), "pos": pos}
+
+
+def gen_prompt(wl: Workload, layer: int, n_rows: int, kind: int = PROMPT_GLOBAL,
+               start: Optional[int] = None) -> dict:
+    """Guidance-prompt Q/K/V of `layer` (the tokenised prompt is not
+    available; Gaussian rows of the prompt's length stand in), placed after the
+    stream at positions start.. (default: right after the first chunk)."""
+    if start is None:
+        start = wl.init_len + wl.chunk
+    pos = np.arange(start, start + n_rows, dtype=np.int32)
+    step = 1000 + kind
+    q = rope_f64(_gauss(_rng(wl, step, layer, T_PROMPT_Q), (n_rows, wl.n_q_heads, wl.head_dim),
+                        wl.scale), pos)
+    k = rope_f64(_gauss(_rng(wl, step, layer, T_PROMPT_K), (n_rows, wl.n_kv_heads, wl.head_dim),
+                        wl.scale), pos)
+    v = _gauss(_rng(wl, step, layer, T_PROMPT_V), (n_rows, wl.n_kv_heads, wl.head_dim), wl.scale)
     return {"q": _to_bits(q), "k": _to_bits(k), "v": _to_bits(v), "pos": pos}
 
 

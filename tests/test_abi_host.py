@@ -150,3 +150,67 @@ def test_topk_argument_checks():
     assert H.lib.hermes_select_topk(FAKE, 10, 0, FAKE, None) == H.EINVAL
     assert H.lib.hermes_select_topk(FAKE, 10, 3, None, None) == H.EINVAL
     assert H.lib.hermes_select_topk(FAKE + 1, 10, 3, FAKE, None) == H.EINVAL
+
+
+@pytest.mark.parametrize("over,code", [
+    ({"summary_mode": 2}, H.EINVAL),
+    ({"reindex_mode": 3}, H.EINVAL),
+    ({"scoring_mode": -1}, H.EINVAL),
+    ({"rope_offset": -1}, H.EINVAL),
+    ({"rope_headroom": -5}, H.EINVAL),
+    ({"rope_theta": float("inf")}, H.EINVAL),
+    ({"summary_mode": 1, "n_q_heads": 16, "n_kv_heads": 16, "head_dim": 128}, H.ENOTSUP),
+])
+def test_init_rejects_bad_extension_config(over, code):
+    cfg = _cfg(**over)
+    rc, ctx = _init(cfg, _bufs(3), nbytes=1 << 30)
+    assert rc == code and not ctx.value
+
+
+def test_extensions_need_rope_buffers_and_room_for_the_summary():
+    # summary or re-indexing without RoPE-position buffers
+    for over in ({"summary_mode": 1}, {"reindex_mode": H.REINDEX_EAGER}):
+        assert _init(_cfg(**over), _bufs(3))[0] == H.EINVAL
+    b = _bufs(3)
+    for l in range(3):
+        b[l].rpos[0] = FAKE
+        b[l].rpos[1] = FAKE + 2            # misaligned
+    assert _init(_cfg(reindex_mode=H.REINDEX_LAZY), b)[0] == H.EINVAL
+    # a deep layer with summaries needs budget + 1 rows (default classes of 3
+    # layers: shallow, middle, deep)
+    b = _bufs(3, cap=8)
+    for l in range(3):
+        b[l].rpos[0] = b[l].rpos[1] = FAKE
+    cfg = _cfg(summary_mode=1, max_cap=8)
+    assert _init(cfg, b)[0] == H.ECAPACITY
+
+
+def test_workspace_grows_with_summary_buffers():
+    base = H.lib.hermes_workspace_bytes(ctypes.byref(_cfg(max_cap=4096)))
+    summ = H.lib.hermes_workspace_bytes(ctypes.byref(_cfg(max_cap=4096, summary_mode=1)))
+    # fp64 block sums: ceil(4096 / 512) blocks x 2 x Hkv*d doubles per layer
+    assert summ - base >= 3 * 8 * 2 * 128 * 8
+
+
+def test_budget_from_weights_matches_oracle():
+    from oracle import hermes_extensions as he
+    from oracle import hermes_oracle as ho
+    cls = ho.layer_partition(28)
+    for wts in ((1.0, 1.0, 1.0), (1.3, 1.0, 0.7), (0.7, 1.6, 0.7), (0.7, 1.0, 1.3)):
+        w = [wts[c] for c in cls]
+        assert H.budget_from_weights(w, 6000 * 28) == he.budget_allocation(w, 6000 * 28)
+    rng = __import__("numpy").random.default_rng(7)
+    for _ in range(20):
+        w = list(rng.uniform(0.1, 3.0, size=24))
+        total = int(rng.integers(24 * 10, 24 * 9000))
+        assert H.budget_from_weights(w, total) == he.budget_allocation(w, total)
+
+
+@pytest.mark.parametrize("weights,total", [
+    ([1.0, float("nan")], 100), ([1.0, -1.0], 100), ([0.0, 0.0], 100), ([1.0, 1.0], 1),
+    ([1e-9, 1.0], 100),           # the first layer would get 0 tokens
+])
+def test_budget_from_weights_rejects(weights, total):
+    with pytest.raises(H.HermesError) as e:
+        H.budget_from_weights(weights, total)
+    assert e.value.code == H.EINVAL

@@ -1,0 +1,306 @@
+"""GPU parity of the adjacent rows through the C ABI: summary tokens,
+eager / lazy RoPE re-indexing, guidance-prompt scoring and the budget helper,
+against the extension oracle on the same seeded inputs.
+
+Kept sets follow the core contract (bit-exact outside the 1e-6 band of the
+budget-th key).  The compacted cache is then rebuilt by the oracle from the
+GPU's own kept set, so near-tie swaps cannot leak into the comparison of the
+summary rows and the rotated keys.  Those are computed in fp64 on both sides
+and stored as bf16 through fp32; the two fp64 values differ only at the 1e-16
+level (pow, sincos, fused multiply-adds, summation order), which changes the
+stored bf16 only when the value sits at a rounding tie.  The bar: every
+element within one bf16 ulp and at most 1e-4 of the elements off by one."""
+from __future__ import annotations
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import hermes_extensions as he
+from oracle import hermes_oracle as orc
+from paper_2601_14724_amd import hermes as H
+from paper_2601_14724_amd import streaming, workloads as wk
+
+from _parity import check_kept, f64, say
+
+pytestmark = pytest.mark.gpu
+
+S, M, D = orc.SHALLOW, orc.MIDDLE, orc.DEEP
+
+
+def _wl(name, wid, L, Hq, Hkv, d, T0, C, budgets, n_steps=1):
+    return wk.custom(name, wid, L, Hq, Hkv, d, T0, C, budgets, n_steps=n_steps)
+
+
+def _ext_caches(caches):
+    return [he.ExtLayerCache(f64(c["k"]), f64(c["v"]), c["pos"].astype(np.int64),
+                             c.get("rpos", c["pos"]).astype(np.int64)) for c in caches]
+
+
+def _ext_chunks(chunks):
+    return [{"q": f64(c["q"]), "k": f64(c["k"]), "v": f64(c["v"]), "pos": c["pos"]} for c in chunks]
+
+
+def _bits(t: torch.Tensor) -> np.ndarray:
+    return t.view(torch.int16).cpu().numpy().view(np.uint16)
+
+
+def _cmp_layer(l, kv, exp: he.ExtLayerCache, what):
+    k, v, p = kv.view(l)
+    rp = kv.view_rope(l)
+    n = len(exp.pos)
+    assert k.shape[0] == n, f"{what} layer {l}: length {k.shape[0]} != {n}"
+    assert np.array_equal(p.cpu().numpy(), exp.pos), f"{what} layer {l}: positions differ"
+    assert np.array_equal(rp.cpu().numpy(), exp.rpos), f"{what} layer {l}: RoPE positions differ"
+    kg = wk.bf16_bits_to_f64(_bits(k).reshape(exp.k.shape))
+    vg = wk.bf16_bits_to_f64(_bits(v).reshape(exp.v.shape))
+    for name, g, e in (("K", kg, exp.k), ("V", vg, exp.v)):
+        diff = g != e
+        if diff.any():
+            ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(e), 1e-30))) - 7)
+            worst = float(np.max(np.abs(g - e)[diff] / ulp[diff]))
+            say(f"{what} layer {l} {name}: {int(diff.sum())} of {diff.size} differ, worst {worst} ulp")
+            assert worst <= 1.0 and diff.mean() <= 1e-4, f"{what} layer {l}: {name} differs"
+
+
+def _run(wl, classes, ext: he.ExtConfig, caches, chunks, prompts=None, **kw):
+    kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, layer_class=classes,
+                              summary_mode=int(ext.summary), reindex_mode=ext.reindex_mode,
+                              rope_offset=ext.rope_offset, rope_limit=ext.rope_limit,
+                              rope_headroom=ext.rope_headroom, rope_theta=ext.rope_theta,
+                              scoring_mode=ext.scoring_mode, **kw)
+    t = streaming.chunk_tensors(_stack(chunks), "cuda")
+    kv.append(t["q"], t["k"], t["v"], t["pos"])
+    if prompts is not None:
+        for l, p in enumerate(prompts):
+            if p is None:
+                continue
+            pt = {k2: streaming.bf16_tensor(p[k2], "cuda") for k2 in ("q", "k", "v")}
+            kv.guidance(pt["q"], pt["k"], pt["v"], layer=l)
+    torch.cuda.synchronize()
+    w = [kv.w[l].cpu().numpy().copy() for l in range(wl.n_layers)]
+    kv.compress()
+    torch.cuda.synchronize()
+    return kv, w
+
+
+def _stack(chunks):
+    return {k: np.stack([c[k] for c in chunks]) for k in ("q", "k", "v")} | {"pos": chunks[0]["pos"]}
+
+
+def _check_step(wl, classes, ext, kv, ref, what):
+    """Kept sets against the oracle, then the compacted caches rebuilt by the
+    oracle from the GPU's kept sets."""
+    compact = []
+    for l in range(wl.n_layers):
+        cat = ref["appended"][l]
+        T = len(cat.pos)
+        if T > wl.budgets[l]:
+            idx = kv.kept_dbg[l].cpu().numpy().astype(np.int64)
+            check_kept(idx, ref["smoothed"][l], wl.budgets[l], f"{what} layer {l}")
+        else:
+            idx = np.arange(T)
+        c, _ = he.compact_layer(cat, idx, classes[l] == D, ext)
+        compact.append(c)
+    compact, reidx = he.reindex_layers(compact, ext)
+    for l in range(wl.n_layers):
+        _cmp_layer(l, kv, compact[l], what)
+    return compact, reidx
+
+
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128)])
+@pytest.mark.parametrize("reindex", [he.REINDEX_NONE, he.REINDEX_EAGER])
+def test_summary_tokens(shape, reindex):
+    Hq, Hkv, d = shape
+    classes = [S, M, D, D]
+    wl = _wl("ext_sum", 40 + d, 4, Hq, Hkv, d, 1024, 196, (512, 600, 512, 700))
+    caches = [wk.gen_cache(wl, l) for l in range(4)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(4)]
+    ext = he.ExtConfig(summary=True, reindex_mode=reindex, rope_offset=11)
+    say(f"summary tokens {shape} reindex {reindex}")
+    kv, _ = _run(wl, classes, ext, caches, chunks)
+    cfg = orc.OracleConfig(budgets=list(wl.budgets), classes=classes)
+    ref = he.stream_step_ext(_ext_caches(caches), _ext_chunks(chunks), cfg, ext)
+    compact, reidx = _check_step(wl, classes, ext, kv, ref, "summary")
+    assert reidx == (reindex == he.REINDEX_EAGER)
+    for l in (2, 3):
+        assert kv.length(l) == wl.budgets[l] + 1
+    kv.close()
+
+
+def test_eager_reindex_in_place_for_layers_within_budget():
+    """Layers that keep everything are re-indexed in their current buffer."""
+    classes = [S, M, D, D]
+    wl = _wl("ext_inplace", 50, 4, 14, 2, 64, 700, 196, (2000, 512, 2000, 512))
+    caches = [wk.gen_cache(wl, l) for l in range(4)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(4)]
+    ext = he.ExtConfig(summary=True, reindex_mode=he.REINDEX_EAGER, rope_offset=3)
+    say("eager re-index, two layers within budget")
+    kv, _ = _run(wl, classes, ext, caches, chunks)
+    cfg = orc.OracleConfig(budgets=list(wl.budgets), classes=classes)
+    ref = he.stream_step_ext(_ext_caches(caches), _ext_chunks(chunks), cfg, ext)
+    _check_step(wl, classes, ext, kv, ref, "in-place")
+    assert kv.length(0) == 896 and kv.length(2) == 896 and kv.length(3) == 513
+    kv.close()
+
+
+@pytest.mark.parametrize("limit,fires", [(1220 + 100, False), (1219 + 100, True)])
+def test_lazy_reindex_trigger(limit, fires):
+    """The largest retained position is 1219 (the chunk's last token is kept
+    by every recency-scored layer); lazy re-indexing fires when
+    1219 + headroom >= limit."""
+    classes = [S, M, D, D]
+    wl = _wl("ext_lazy", 51, 4, 14, 2, 64, 1024, 196, (512, 512, 512, 512))
+    caches = [wk.gen_cache(wl, l) for l in range(4)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(4)]
+    ext = he.ExtConfig(summary=True, reindex_mode=he.REINDEX_LAZY, rope_offset=0,
+                       rope_limit=limit, rope_headroom=100)
+    say(f"lazy re-index limit {limit}")
+    kv, _ = _run(wl, classes, ext, caches, chunks)
+    cfg = orc.OracleConfig(budgets=list(wl.budgets), classes=classes)
+    ref = he.stream_step_ext(_ext_caches(caches), _ext_chunks(chunks), cfg, ext)
+    _, reidx = _check_step(wl, classes, ext, kv, ref, "lazy")
+    assert reidx == fires
+    kv.close()
+
+
+def test_stream_with_summaries_and_eager_reindex():
+    """Four successive chunks; after each step the oracle continues from the
+    GPU's compacted state read back from the device, so an element one ulp off
+    at one step cannot drift further at the next."""
+    classes = [S, M, M, D, D]
+    L, C = 5, 196
+    wl = _wl("ext_stream", 52, L, 14, 2, 64, 600, C, (700, 650, 600, 640, 560), n_steps=4)
+    caches = [wk.gen_cache(wl, l) for l in range(L)]
+    ext = he.ExtConfig(summary=True, reindex_mode=he.REINDEX_EAGER, rope_offset=5)
+    kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, layer_class=classes,
+                              summary_mode=1, reindex_mode=he.REINDEX_EAGER, rope_offset=5)
+    cfg = orc.OracleConfig(budgets=list(wl.budgets), classes=classes)
+    state = _ext_caches(caches)
+    for step in range(4):
+        chunks = [wk.gen_chunk(wl, step, l) for l in range(L)]
+        # after re-indexing the next chunk's keys would be rotated at positions
+        # following the re-indexed cache; the stream positions serve as both
+        # here, which only needs them to exceed every retained RoPE position
+        say(f"stream step {step}")
+        t = streaming.chunk_tensors(_stack(chunks), "cuda")
+        kv.append(t["q"], t["k"], t["v"], t["pos"])
+        kv.compress()
+        torch.cuda.synchronize()
+        ref = he.stream_step_ext(state, _ext_chunks(chunks), cfg, ext)
+        _check_step(wl, classes, ext, kv, ref, f"step {step}")
+        state = _gpu_state(kv, L)     # continue from the GPU's exact state
+    kv.close()
+
+
+def _gpu_state(kv, L):
+    out = []
+    for l in range(L):
+        k, v, p = kv.view(l)
+        shp = (k.shape[0], k.shape[1], k.shape[2])
+        out.append(he.ExtLayerCache(wk.bf16_bits_to_f64(_bits(k).reshape(shp)),
+                                    wk.bf16_bits_to_f64(_bits(v).reshape(shp)),
+                                    p.cpu().numpy().astype(np.int64),
+                                    kv.view_rope(l).cpu().numpy().astype(np.int64)))
+    return out
+
+
+def test_guidance_prompt_scoring():
+    """W from guidance rows (global prompt for deep layers, hybrid prompt for
+    middle layers), then scoring, smoothing and selection."""
+    classes = [S, M, M, D, D]
+    L = 5
+    wl = _wl("ext_guide", 53, L, 14, 2, 64, 1024, 196, (512, 600, 550, 512, 640))
+    caches = [wk.gen_cache(wl, l) for l in range(L)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(L)]
+    n_rows = {M: 40, D: 24}
+    prompts = [None if classes[l] == S else
+               wk.gen_prompt(wl, l, n_rows[classes[l]],
+                             wk.PROMPT_HYBRID if classes[l] == M else wk.PROMPT_GLOBAL)
+               for l in range(L)]
+    ext = he.ExtConfig(scoring_mode=he.SCORE_GUIDANCE)
+    say("guidance-prompt scoring")
+    kv, w = _run(wl, classes, ext, caches, chunks, prompts=prompts)
+    cfg = orc.OracleConfig(budgets=list(wl.budgets), classes=classes)
+    pr = [None if p is None else {"q": f64(p["q"]), "k": f64(p["k"]), "v": f64(p["v"])}
+          for p in prompts]
+    ref = he.stream_step_ext(_ext_caches(caches), _ext_chunks(chunks), cfg, ext, prompts=pr)
+    for l in range(L):
+        T = len(ref["appended"][l].pos)
+        if classes[l] != S:
+            rel = float(np.max(np.abs(w[l][:T] - ref["w"][l]) / ref["w"][l]))
+            say(f"layer {l}: W rel {rel:.2e}")
+            assert rel <= 1e-3
+            sg = kv.s_dbg[l][:T].cpu().numpy().astype(np.float64)
+            srel = float(np.max(np.abs(sg - ref["smoothed"][l]) / ref["smoothed"][l]))
+            assert srel <= 1e-3, f"layer {l}: smoothed key rel {srel}"
+        idx = kv.kept_dbg[l].cpu().numpy().astype(np.int64)
+        check_kept(idx, ref["smoothed"][l], wl.budgets[l], f"guidance layer {l}")
+    kv.close()
+
+
+def test_guidance_state_errors():
+    classes = [S, M, D]
+    wl = _wl("ext_guide_err", 54, 3, 14, 2, 64, 300, 64, (200, 200, 200))
+    caches = [wk.gen_cache(wl, l) for l in range(3)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(3)]
+    t = streaming.chunk_tensors(_stack(chunks), "cuda")
+    p = wk.gen_prompt(wl, 2, 16)
+    pt = {k2: streaming.bf16_tensor(p[k2], "cuda") for k2 in ("q", "k", "v")}
+    # chunk scoring: the guidance entry point is refused
+    kv = streaming.make_cache(wl, device="cuda", caches=caches, layer_class=classes)
+    kv.append(t["q"], t["k"], t["v"], t["pos"])
+    with pytest.raises(H.HermesError) as e:
+        kv.guidance(pt["q"], pt["k"], pt["v"], layer=2)
+    assert e.value.code == H.ESTATE
+    kv.close()
+    # guidance scoring: compress needs the prompt mass of layers 1 and 2
+    kv = streaming.make_cache(wl, device="cuda", caches=caches, layer_class=classes,
+                              scoring_mode=H.SCORE_GUIDANCE)
+    with pytest.raises(H.HermesError) as e:       # not appended yet
+        kv.guidance(pt["q"], pt["k"], pt["v"], layer=2)
+    assert e.value.code == H.ESTATE
+    kv.append(t["q"], t["k"], t["v"], t["pos"])
+    kv.guidance(pt["q"], pt["k"], pt["v"], layer=2)
+    with pytest.raises(H.HermesError) as e:       # layer 1 missing
+        kv.compress()
+    assert e.value.code == H.ESTATE
+    p1 = wk.gen_prompt(wl, 1, 16)
+    kv.guidance(*(streaming.bf16_tensor(p1[k2], "cuda") for k2 in ("q", "k", "v")), layer=1)
+    kv.compress()
+    torch.cuda.synchronize()
+    assert [kv.length(l) for l in range(3)] == [200, 200, 200]
+    kv.close()
+
+
+def test_fullsize_7b_summary_and_eager_reindex():
+    """28 layers at the 7B shape (8192 cached + 784 new, budgets 2048..6144)
+    with summaries and eager re-indexing: every layer's compacted cache,
+    rebuilt by the oracle from the GPU's kept set, matches bit for bit."""
+    wl = wk.WORKLOADS["c3_7b_28layer"]
+    classes = orc.layer_partition(wl.n_layers)
+    say("c3 full size: generating inputs")
+    caches = [wk.gen_cache(wl, l) for l in range(wl.n_layers)]
+    st = wk.stack_chunks(wl, 0)
+    ext = he.ExtConfig(summary=True, reindex_mode=he.REINDEX_EAGER, rope_offset=14)
+    kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, summary_mode=1,
+                              reindex_mode=he.REINDEX_EAGER, rope_offset=14)
+    t = streaming.chunk_tensors(st, "cuda")
+    kv.append(t["q"], t["k"], t["v"], t["pos"])
+    kv.compress()
+    torch.cuda.synchronize()
+    say("c3 full size: comparing")
+    compact = []
+    for l in range(wl.n_layers):
+        cat = he.ExtLayerCache(np.concatenate([f64(caches[l]["k"]), f64(st["k"][l])]),
+                               np.concatenate([f64(caches[l]["v"]), f64(st["v"][l])]),
+                               np.concatenate([caches[l]["pos"], st["pos"]]).astype(np.int64),
+                               np.concatenate([caches[l]["pos"], st["pos"]]).astype(np.int64))
+        idx = kv.kept_dbg[l].cpu().numpy().astype(np.int64)
+        assert len(idx) == wl.budgets[l] and np.all(np.diff(idx) > 0)
+        c, _ = he.compact_layer(cat, idx, classes[l] == D, ext)
+        compact.append(c)
+    compact, _ = he.reindex_layers(compact, ext)
+    for l in range(wl.n_layers):
+        _cmp_layer(l, kv, compact[l], "c3")
+    kv.close()
