@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # and WRITE_SIZE counter passes in profiles/traffic_c3_7b_28layer.md (fetch
 # scaled x2.000, write x1.000 by a 256 MiB copy).  Valid only for the kernel
 # source it was measured on: reported as null once attention.hip changes.
-ATTN_TRAFFIC = {"bytes": 1.4206e9, "source_sha256_16": "bdbca8703662e1bd",
+ATTN_TRAFFIC = {"bytes": 1.4166e9, "source_sha256_16": "421d07fa6297ff7e",
                 "workload": "c3_7b_28layer"}
 
 
@@ -104,6 +104,8 @@ def main() -> int:
     ap.add_argument("--workload", default="c3_7b_28layer")
     ap.add_argument("--cpu-sample-layers", type=int, default=4)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extensions", action="store_true",
+                    help="skip the summary-token / re-indexing / guidance-prompt timings")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -127,7 +129,7 @@ def main() -> int:
     st = {k: np.stack([c[k] for c in chunks]) for k in ("q", "k", "v")} | {"pos": chunks[0]["pos"]}
     t = streaming.chunk_tensors(st, dev)
     out = torch.empty_like(t["q"])
-    del caches, chunks, st
+    del chunks, st
 
     def step():
         kv.rewind()
@@ -180,6 +182,11 @@ def main() -> int:
     if "colsum" in kernels:
         sweep = attention_flops(wl) / 2 * _mass_layer_fraction(wl)
         extra["colsum_TFLOPs_executed"] = round(sweep / (kernels["colsum"]["avg_ms"] * 1e-3) / 1e12, 2)
+    kv.close()
+    ext = None
+    if not args.no_extensions:
+        log("[bench] adjacent rows: summary tokens + eager re-indexing, guidance prompt")
+        ext = extension_bench(wl, caches, t, args.steps, args.warmup)
     cpu = None
     if not args.no_cpu_baseline:
         log(f"[bench] oracle CPU baseline on {args.cpu_sample_layers} layers")
@@ -194,9 +201,76 @@ def main() -> int:
                       "budgets": f"{wl.budgets[0]}..{wl.budgets[-1]} (linear ramp)",
                       "parallelism": "single GPU"},
            "roofline": roofline, "cpu_baseline": cpu, **extra}
+    if ext is not None:
+        rec["extensions"] = ext
     print(json.dumps(rec), flush=True)
-    kv.close()
     return 0
+
+
+def extension_bench(wl, caches, t, steps: int, warmup: int, prompt_rows: int = 64) -> dict:
+    """The adjacent rows on the same workload: (a) summary tokens in the deep
+    layers plus eager RoPE re-indexing at every compression, (b) W from a
+    guidance prompt of `prompt_rows` tokens per non-shallow layer instead of
+    the chunk.  Reports step time and per-kernel averages."""
+    import torch
+
+    from paper_2601_14724_amd import hermes as H
+    from paper_2601_14724_amd import streaming, workloads as wk
+    out = {}
+    dev = t["q"].device
+
+    def timed(kv, step):
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        kv.profile(True)
+        for kid in range(len(H.KERNEL_NAMES)):
+            kv.profile_read(kid)
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            step()
+        torch.cuda.synchronize()
+        dt = (time.perf_counter() - t0) / steps
+        ks = {}
+        for kid, name in enumerate(H.KERNEL_NAMES):
+            ms, cnt = kv.profile_read(kid)
+            if cnt:
+                ks[name] = round(ms / cnt, 4)
+        kv.profile(False)
+        return dt, ks
+
+    o = torch.empty_like(t["q"])
+    kv = streaming.make_cache(wl, device=dev, caches=caches, summary_mode=1,
+                              reindex_mode=H.REINDEX_EAGER, rope_offset=14)
+
+    def step_a():
+        kv.rewind()
+        kv.append(t["q"], t["k"], t["v"], t["pos"], out=o)
+        kv.compress()
+    dt, ks = timed(kv, step_a)
+    row = wl.n_kv_heads * wl.head_dim * 2
+    kept = sum(b + 1 if i >= wl.n_layers - int(np.floor(0.3 * wl.n_layers + 0.5)) else b
+               for i, b in enumerate(wl.budgets))
+    g = kept * (4.0 * row + 16.0) / (ks["gather"] * 1e-3) / 1e9 if "gather" in ks else None
+    out["summary_eager_reindex"] = {"ms_per_step": round(dt * 1e3, 4), "kernels_ms": ks,
+                                    "gather_rotate_GBps": round(g, 1) if g else None}
+    kv.close()
+    del kv
+
+    kv = streaming.make_cache(wl, device=dev, caches=caches, scoring_mode=H.SCORE_GUIDANCE)
+    pr = [wk.gen_prompt(wl, l, prompt_rows) for l in range(wl.n_layers)]
+    pt = {k: streaming.bf16_tensor(np.stack([p[k] for p in pr]), dev) for k in ("q", "k", "v")}
+
+    def step_b():
+        kv.rewind()
+        kv.append(t["q"], t["k"], t["v"], t["pos"], out=o)
+        kv.guidance(pt["q"], pt["k"], pt["v"])
+        kv.compress()
+    dt, ks = timed(kv, step_b)
+    out["guidance_prompt"] = {"ms_per_step": round(dt * 1e3, 4), "prompt_rows": prompt_rows,
+                              "kernels_ms": ks}
+    kv.close()
+    return out
 
 
 def _mass_layer_fraction(wl) -> float:
