@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # and WRITE_SIZE counter passes in profiles/traffic_c3_7b_28layer.md (fetch
 # scaled x2.000, write x1.000 by a 256 MiB copy).  Valid only for the kernel
 # source it was measured on: reported as null once attention.hip changes.
-ATTN_TRAFFIC = {"bytes": 1.4166e9, "source_sha256_16": "421d07fa6297ff7e",
+ATTN_TRAFFIC = {"bytes": 1.4225e9, "source_sha256_16": "6579f46e6310ab88",
                 "workload": "c3_7b_28layer"}
 
 
@@ -182,6 +182,7 @@ def main() -> int:
     if "colsum" in kernels:
         sweep = attention_flops(wl) / 2 * _mass_layer_fraction(wl)
         extra["colsum_TFLOPs_executed"] = round(sweep / (kernels["colsum"]["avg_ms"] * 1e-3) / 1e12, 2)
+    qres = query_bench(wl, kv, args.steps, args.warmup)
     kv.close()
     ext = None
     if not args.no_extensions:
@@ -201,10 +202,46 @@ def main() -> int:
                       "budgets": f"{wl.budgets[0]}..{wl.budgets[-1]} (linear ramp)",
                       "parallelism": "single GPU"},
            "roofline": roofline, "cpu_baseline": cpu, **extra}
+    rec["query"] = qres
     if ext is not None:
         rec["extensions"] = ext
     print(json.dumps(rec), flush=True)
     return 0
+
+
+def query_bench(wl, kv, steps: int, warmup: int, n_q: int = 64) -> dict:
+    """Query-time attention: n_q text tokens over every layer's compacted cache
+    (and their own earlier tokens).  Algorithmic work 4 d per visible (row,
+    key, head) triple; bytes = the compacted K/V read once + Q and O."""
+    import torch
+
+    from paper_2601_14724_amd import hermes as H
+    from paper_2601_14724_amd import streaming, workloads as wk
+    qw = wk.scaled(wl, query_len=n_q)
+    qs = [wk.gen_query(qw, l) for l in range(wl.n_layers)]
+    dev = kv.device
+    qt = {k: streaming.bf16_tensor(np.stack([q[k] for q in qs]), dev) for k in ("q", "k", "v")}
+    o = torch.empty_like(qt["q"])
+    lens = [kv.length(l) for l in range(wl.n_layers)]
+    for _ in range(warmup):
+        kv.query(qt["q"], qt["k"], qt["v"], out=o)
+    torch.cuda.synchronize()
+    kv.profile(True)
+    kv.profile_read(H.K_QUERY)
+    for _ in range(steps):
+        kv.query(qt["q"], qt["k"], qt["v"], out=o)
+    ms, cnt = kv.profile_read(H.K_QUERY)
+    kv.profile(False)
+    ms /= max(cnt, 1)
+    pairs = wl.n_q_heads * sum(n_q * T + n_q * (n_q + 1) // 2 for T in lens)
+    flops = 4.0 * wl.head_dim * pairs
+    row = wl.n_kv_heads * wl.head_dim * 2
+    nbytes = sum(lens) * 2 * row + wl.n_layers * n_q * (2 * wl.n_q_heads * wl.head_dim * 2 + 2 * row)
+    tf = flops / (ms * 1e-3) / 1e12
+    gb = nbytes / (ms * 1e-3) / 1e9
+    return {"n_q": n_q, "cache_tokens": sum(lens), "ms": round(ms, 4),
+            "TFLOPs": round(tf, 2), "mfma_frac": round(tf / PEAK_BF16_TFLOPS, 4),
+            "GBps": round(gb, 1), "hbm_frac": round(gb / PEAK_HBM_GBS, 4)}
 
 
 def extension_bench(wl, caches, t, steps: int, warmup: int, prompt_rows: int = 64) -> dict:

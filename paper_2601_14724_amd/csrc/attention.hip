@@ -67,12 +67,19 @@ __device__ __forceinline__ int xcd_remap(int i, int n) {
   return x < r ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
 }
 
-template <int D>
+// SPLIT: one key slice per workgroup, partial state out (see AttnArgs).
+// WRITE_O: store O (chunk and query passes); without it only the row LSE is
+// written (guidance-prompt passes).
+template <int D, bool SPLIT, bool WRITE_O>
 __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
+  // Consecutive ids: the query tiles of one (layer, KV head[, key slice]),
+  // which stream the same K/V.
+  const int nsp = SPLIT ? a.nsplit : 1;
   const int qtile = lin % nqt;
-  const int kv = (lin / nqt) % a.Hkv;
-  const int j = lin / (nqt * a.Hkv);
+  const int split = SPLIT ? (lin / nqt) % nsp : 0;
+  const int kv = SPLIT ? (lin / (nqt * nsp)) % a.Hkv : (lin / nqt) % a.Hkv;
+  const int j = SPLIT ? lin / (nqt * nsp * a.Hkv) : lin / (nqt * a.Hkv);
   const int layer = a.layer_id[j];
   const LayerTable &lt = a.tab[layer];
   const int cur = a.cur[j];
@@ -91,7 +98,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   const uint16_t *q = a.q + slot * a.q_lstride;
   const uint16_t *kn = a.kn + slot * a.kv_lstride;
   const uint16_t *vn = a.vn + slot * a.kv_lstride;
-  uint16_t *out = a.out != nullptr ? a.out + slot * a.q_lstride : nullptr;
+  uint16_t *out = a.out + slot * a.q_lstride;
   const uint16_t *kc = lt.k[cur];
   const uint16_t *vc = lt.v[cur];
 
@@ -254,43 +261,125 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
 
   using NoMask = std::integral_constant<bool, false>;
   using Mask = std::integral_constant<bool, true>;
-  if (n_pure > 0) load_pure(0); else load_any(0);
-  for (int t = 0; t < n_pure; ++t) {
-    store_tile(t & 1);
-    __syncthreads();
-    if (t + 1 < n_pure) load_pure((t + 1) * BN);
-    else if (t + 1 < ntiles) load_any((t + 1) * BN);
-    compute(t, NoMask{});
-  }
-  for (int t = n_pure; t < ntiles; ++t) {
-    store_tile(t & 1);
-    __syncthreads();
-    if (t + 1 < ntiles) load_any((t + 1) * BN);
-    if ((t + 1) * BN - 1 > vis_min) compute(t, Mask{}); else compute(t, NoMask{});
+  if constexpr (!SPLIT) {
+    if (n_pure > 0) load_pure(0); else load_any(0);
+    for (int t = 0; t < n_pure; ++t) {
+      store_tile(t & 1);
+      __syncthreads();
+      if (t + 1 < n_pure) load_pure((t + 1) * BN);
+      else if (t + 1 < ntiles) load_any((t + 1) * BN);
+      compute(t, NoMask{});
+    }
+    for (int t = n_pure; t < ntiles; ++t) {
+      store_tile(t & 1);
+      __syncthreads();
+      if (t + 1 < ntiles) load_any((t + 1) * BN);
+      if ((t + 1) * BN - 1 > vis_min) compute(t, Mask{}); else compute(t, NoMask{});
+    }
+  } else {
+    // this workgroup's slice [t_begin, t_end) of the key tiles
+    const int tps = (ntiles + nsp - 1) / nsp;
+    const int t_begin = min(ntiles, split * tps);
+    const int t_end = min(ntiles, t_begin + tps);
+    const int p_end = min(n_pure, t_end);
+    int t = t_begin;
+    if (t < t_end) {
+      if (t < p_end) load_pure(t * BN); else load_any(t * BN);
+    }
+    for (; t < p_end; ++t) {
+      store_tile(t & 1);
+      __syncthreads();
+      if (t + 1 < p_end) load_pure((t + 1) * BN);
+      else if (t + 1 < t_end) load_any((t + 1) * BN);
+      compute(t, NoMask{});
+    }
+    for (; t < t_end; ++t) {
+      store_tile(t & 1);
+      __syncthreads();
+      if (t + 1 < t_end) load_any((t + 1) * BN);
+      if ((t + 1) * BN - 1 > vis_min) compute(t, Mask{}); else compute(t, NoMask{});
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if constexpr (SPLIT) {
+    // unnormalised partial state of this key slice
+    if (row_ok) {
+      const int64_t row = ((int64_t)(j * Hkv + kv) * nsp + split) * a.part_rows + prow;
+      float *op = a.opart + row * D;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int grp = 0; grp < 4; ++grp) {
+          const int d0 = 32 * db + 8 * grp + 4 * half;
+          *reinterpret_cast<float4 *>(op + d0) =
+              float4{o[db][4 * grp], o[db][4 * grp + 1], o[db][4 * grp + 2], o[db][4 * grp + 3]};
+        }
+      if (half == 0) *reinterpret_cast<float2 *>(a.mlpart + 2 * row) = float2{m_run, l_tot};
+    }
+    return;
+  }
   const float inv = 1.f / l_tot;
-  if (row_ok && out != nullptr) {
-    uint16_t *orow = out + ((int64_t)r * Hq + h) * D;
+  if (row_ok) {
+    if constexpr (WRITE_O) {
+      uint16_t *orow = out + ((int64_t)r * Hq + h) * D;
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
+      for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
-      for (int grp = 0; grp < 4; ++grp) {
-        const int d0 = 32 * db + 8 * grp + 4 * half;
-        const uint32_t w0 = (uint32_t)f2bf(o[db][4 * grp + 0] * inv) |
-                            ((uint32_t)f2bf(o[db][4 * grp + 1] * inv) << 16);
-        const uint32_t w1 = (uint32_t)f2bf(o[db][4 * grp + 2] * inv) |
-                            ((uint32_t)f2bf(o[db][4 * grp + 3] * inv) << 16);
-        *reinterpret_cast<uint2 *>(orow + d0) = uint2{w0, w1};
+        for (int grp = 0; grp < 4; ++grp) {
+          const int d0 = 32 * db + 8 * grp + 4 * half;
+          const uint32_t w0 = (uint32_t)f2bf(o[db][4 * grp + 0] * inv) |
+                              ((uint32_t)f2bf(o[db][4 * grp + 1] * inv) << 16);
+          const uint32_t w1 = (uint32_t)f2bf(o[db][4 * grp + 2] * inv) |
+                              ((uint32_t)f2bf(o[db][4 * grp + 3] * inv) << 16);
+          *reinterpret_cast<uint2 *>(orow + d0) = uint2{w0, w1};
+        }
       }
     }
-  }
-  if (row_ok && a.lse != nullptr && half == 0) {
-    a.lse[layer * a.lse_lstride + (int64_t)kv * P + prow] = m_run + log2f(l_tot);
+    if (a.lse != nullptr && half == 0) {
+      a.lse[layer * a.lse_lstride + (int64_t)kv * P + prow] = m_run + log2f(l_tot);
+    }
   }
 }
 
+
+// Merge of the key slices: m = max_s m_s, w_s = 2^(m_s - m),
+// O = sum_s w_s O_s / sum_s w_s l_s, LSE = m + log2(sum_s w_s l_s).
+// One thread per (packed row, 8 channels), slices summed in order.
+template <int D>
+__global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
+  const int j = blockIdx.z, kv = blockIdx.y;
+  const int layer = a.layer_id[j];
+  const int G = a.Hq / a.Hkv, P = a.C * G, nsp = a.nsplit;
+  const int e = blockIdx.x * 256 + threadIdx.x;
+  if (e >= P * (D / 8)) return;
+  const int p = e / (D / 8), c8 = e % (D / 8);
+  const int64_t row0 = (int64_t)(j * a.Hkv + kv) * nsp * a.part_rows + p;
+  float m = -INFINITY;
+  for (int s = 0; s < nsp; ++s) m = fmaxf(m, a.mlpart[2 * (row0 + (int64_t)s * a.part_rows)]);
+  float lsum = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < nsp; ++s) {
+    const int64_t row = row0 + (int64_t)s * a.part_rows;
+    const float w = exp2f(a.mlpart[2 * row] - m);
+    lsum += w * a.mlpart[2 * row + 1];
+    const float4 x0 = *reinterpret_cast<const float4 *>(a.opart + row * D + 8 * c8);
+    const float4 x1 = *reinterpret_cast<const float4 *>(a.opart + row * D + 8 * c8 + 4);
+    acc[0] += w * x0.x; acc[1] += w * x0.y; acc[2] += w * x0.z; acc[3] += w * x0.w;
+    acc[4] += w * x1.x; acc[5] += w * x1.y; acc[6] += w * x1.z; acc[7] += w * x1.w;
+  }
+  const int r = p / G, h = kv * G + (p - r * G);
+  if (a.out != nullptr) {
+    const float inv = 1.f / lsum;
+    uint16_t *orow = a.out + a.slot[j] * a.q_lstride + ((int64_t)r * a.Hq + h) * D + 8 * c8;
+    uint32_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = (uint32_t)f2bf(acc[2 * i] * inv) | ((uint32_t)f2bf(acc[2 * i + 1] * inv) << 16);
+    *reinterpret_cast<uint4 *>(orow) = uint4{w[0], w[1], w[2], w[3]};
+  }
+  if (a.lse != nullptr && c8 == 0)
+    a.lse[layer * a.lse_lstride + (int64_t)kv * P + p] = m + log2f(lsum);
+}
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
@@ -496,10 +585,32 @@ hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStre
   const int P = a.C * (a.Hq / a.Hkv);
   const int nqt = (P + BM - 1) / BM;
   dim3 grid(nqt * a.Hkv * n_list);
+  const bool wo = a.out != nullptr;
   if (head_dim == 64) {
-    hipLaunchKernelGGL(attn_fwd<64>, grid, dim3(256), 0, s, a, nqt);
+    if (wo) hipLaunchKernelGGL((attn_fwd<64, false, true>), grid, dim3(256), 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<64, false, false>), grid, dim3(256), 0, s, a, nqt);
   } else {
-    hipLaunchKernelGGL(attn_fwd<128>, grid, dim3(256), 0, s, a, nqt);
+    if (wo) hipLaunchKernelGGL((attn_fwd<128, false, true>), grid, dim3(256), 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<128, false, false>), grid, dim3(256), 0, s, a, nqt);
+  }
+  return hipGetLastError();
+}
+
+hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, hipStream_t s) {
+  const int P = a.C * (a.Hq / a.Hkv);
+  const int nqt = (P + BM - 1) / BM;
+  dim3 grid(nqt * a.nsplit * a.Hkv * n_list);
+  dim3 cgrid((P * (head_dim / 8) + 255) / 256, a.Hkv, n_list);
+  if (head_dim == 64) {
+    hipLaunchKernelGGL((attn_fwd<64, true, true>), grid, dim3(256), 0, s, a, nqt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_combine<64>, cgrid, dim3(256), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((attn_fwd<128, true, true>), grid, dim3(256), 0, s, a, nqt);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(attn_combine<128>, cgrid, dim3(256), 0, s, a);
   }
   return hipGetLastError();
 }

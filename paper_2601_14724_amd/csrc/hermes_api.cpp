@@ -23,8 +23,9 @@ size_t round_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t tab, lse, keys, kept, wpart, spart, sumk, sumv, smeta, flag, total;
+  size_t tab, lse, keys, kept, wpart, spart, sumk, sumv, smeta, flag, opart, mlpart, total;
   int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride;
+  int32_t part_rows;
 };
 
 int max_budget(const hermes_config *c) {
@@ -100,8 +101,29 @@ Layout layout_of(const hermes_config *c) {
   off = round_up(off + sizeof(int32_t) * 4 * (size_t)c->n_layers);
   s.flag = off;
   off = round_up(off + sizeof(int32_t) * 4);
+  // split-key partial state of short passes (query, guidance prompt)
+  s.part_rows = kSplitMaxTokens * (c->n_q_heads / c->n_kv_heads);
+  const size_t prow = (size_t)c->n_layers * c->n_kv_heads * kMaxSplits * s.part_rows;
+  s.opart = off;
+  off = round_up(off + sizeof(float) * prow * c->head_dim);
+  s.mlpart = off;
+  off = round_up(off + sizeof(float) * prow * 2);
   s.total = off;
   return s;
+}
+
+// Key slices for a pass of n_rows rows over caches of at most max_T0 tokens:
+// enough workgroups to fill the GPU, each slice at least 8 key tiles; 1 means
+// the plain kernel.
+int split_count(int n_rows, int G, int Hkv, int n_list, int max_T0) {
+  if (n_rows > kSplitMaxTokens) return 1;
+  const int nqt = (n_rows * G + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
+  const int base = nqt * Hkv * n_list;
+  const int want = (1024 + base - 1) / base;
+  const int tiles = (max_T0 + n_rows + 63) / 64;
+  int s = want < kMaxSplits ? want : kMaxSplits;
+  if (s > tiles / 8) s = tiles / 8;
+  return s < 1 ? 1 : s;
 }
 
 // 10% shallow, 60% middle, 30% deep (Sec. 4.1), rounded to nearest layer.
@@ -596,8 +618,13 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
     max_T = ctx->len[l] > max_T ? ctx->len[l] : max_T;
   }
   const int n = (int)list.size();
+  at.nsplit = split_count(n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, max_T);
+  at.part_rows = ctx->lay.part_rows;
+  at.opart = reinterpret_cast<float *>(ctx->ws + ctx->lay.opart);
+  at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
   const int rc = ctx->run(HERMES_K_GUIDE, s, [&] {
-    hipError_t e = launch_attention(at, n, ctx->D, s);
+    hipError_t e = at.nsplit > 1 ? launch_attention_split(at, n, ctx->D, s)
+                                 : launch_attention(at, n, ctx->D, s);
     if (e != hipSuccess) return e;
     return launch_colsum(cs, n, max_T, ctx->D, s);
   });
@@ -788,16 +815,24 @@ int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   at.Hkv = ctx->Hkv;
   at.C = n_q;
   at.scale_log2 = (float)(ctx->sm_scale * kLog2e);
-  int n = 0;
+  int n = 0, max_T0 = 0;
   for (int l = 0; l < L; ++l) {
     if (layer != HERMES_ALL_LAYERS && l != layer) continue;
     at.T0[n] = ctx->len[l];
     at.layer_id[n] = (int8_t)l;
     at.slot[n] = (int8_t)(layer == HERMES_ALL_LAYERS ? l : 0);
     at.cur[n] = ctx->cur[l];
+    max_T0 = ctx->len[l] > max_T0 ? ctx->len[l] : max_T0;
     ++n;
   }
-  return ctx->run(HERMES_K_QUERY, s, [&] { return launch_attention(at, n, ctx->D, s); });
+  at.nsplit = split_count(n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, max_T0);
+  at.part_rows = ctx->lay.part_rows;
+  at.opart = reinterpret_cast<float *>(ctx->ws + ctx->lay.opart);
+  at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
+  return ctx->run(HERMES_K_QUERY, s, [&] {
+    return at.nsplit > 1 ? launch_attention_split(at, n, ctx->D, s)
+                         : launch_attention(at, n, ctx->D, s);
+  });
 }
 
 int hermes_select_topk(const float *keys, int32_t n, int32_t k, int32_t *out_idx, void *stream) {

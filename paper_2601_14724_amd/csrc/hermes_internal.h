@@ -44,6 +44,13 @@ struct AttnArgs {
   int8_t layer_id[kMaxLayers];
   int8_t slot[kMaxLayers];      // index of the layer's inputs in the stacked tensors
   int8_t cur[kMaxLayers];
+  // Split-key mode (short passes): each workgroup covers one of nsplit slices
+  // of the key tiles and writes unnormalised O, the running maximum and the
+  // row sum to opart / mlpart [entry][Hkv][nsplit][part_rows]; a combine
+  // kernel merges the slices.
+  int32_t nsplit, part_rows;
+  float *opart;             // [..][part_rows][d] fp32
+  float *mlpart;            // [..][part_rows][2] fp32 (max, sum)
 };
 
 // Attention-mass sweep: W_i for the candidates i < ncand[j] of layer
@@ -158,6 +165,7 @@ struct AppendArgs {
 
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);
+hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);
 hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_dim,
                          hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
@@ -172,5 +180,7 @@ hipError_t launch_gather_rope(const GatherArgs &a, hipStream_t s);
 constexpr int kAttnRowsPerBlock = 128;   // packed (row, head) pairs per workgroup
 constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the sweep
 constexpr int kSummaryRows = 512;        // candidates per workgroup of the summary sums
+constexpr int kSplitMaxTokens = 64;      // passes of at most this many rows use split keys
+constexpr int kMaxSplits = 4;
 
 }  // namespace hermes
