@@ -17,6 +17,7 @@
 #include <type_traits>
 
 #include "hermes_internal.h"
+#include "score_terms.h"
 
 namespace hermes {
 namespace {
@@ -567,16 +568,35 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
 }
 
 // W_i = sum over KV heads of the per-head partial masses, in head order.
-__global__ __launch_bounds__(256) void mass_reduce(ColsumArgs a) {
+// W_i = the head-order sum of the per-head fp64 partials, rounded to fp32;
+// with it, per block of kNormBlock candidates, the fp64 partial of the
+// attention-score normaliser sum_i alpha_i W_i over the rounded W (thread
+// order within each wave by a fixed butterfly, then the waves in order).
+__global__ __launch_bounds__(kNormBlock) void mass_reduce(ColsumArgs a) {
   const int j = blockIdx.y;
   const int layer = a.layer_id[j];
   const int T = a.ncand[j];
-  const int i = blockIdx.x * 256 + threadIdx.x;
-  if (i >= T) return;
-  const double *part = a.wpart + layer * a.wpart_lstride + i;
-  double w = 0.0;
-  for (int kv = 0; kv < a.Hkv; ++kv) w += part[(int64_t)kv * a.wpart_hstride];
-  a.tab[layer].w[i] = (float)w;
+  if (blockIdx.x * kNormBlock >= T) return;   // whole block past this layer's end
+  const int i = blockIdx.x * kNormBlock + threadIdx.x;
+  double m = 0.0;
+  if (i < T) {
+    const double *part = a.wpart + layer * a.wpart_lstride + i;
+    double w = 0.0;
+    for (int kv = 0; kv < a.Hkv; ++kv) w += part[(int64_t)kv * a.wpart_hstride];
+    const float wf = (float)w;
+    a.tab[layer].w[i] = wf;
+    m = mass_over_observers(wf, i, a.T0[j], a.C, a.alpha_mode[j]);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) m += __shfl_xor(m, o);
+  __shared__ double red[kNormBlock / 64];
+  if ((threadIdx.x & 63) == 0) red[threadIdx.x >> 6] = m;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double s = 0.0;
+    for (int w = 0; w < kNormBlock / 64; ++w) s += red[w];
+    a.normpart[layer * a.normpart_lstride + blockIdx.x] = s;
+  }
 }
 
 }  // namespace
@@ -626,7 +646,7 @@ hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_di
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(mass_reduce, dim3((max_T + 255) / 256, n_list), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(mass_reduce, dim3((max_T + kNormBlock - 1) / kNormBlock, n_list), dim3(kNormBlock), 0, s, a);
   return hipGetLastError();
 }
 

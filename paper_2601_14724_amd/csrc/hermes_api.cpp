@@ -23,8 +23,8 @@ size_t round_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t tab, lse, keys, kept, wpart, spart, sumk, sumv, smeta, flag, opart, mlpart, total;
-  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride;
+  size_t tab, lse, keys, kept, normpart, wpart, spart, sumk, sumv, smeta, flag, opart, mlpart, total;
+  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride, normpart_lstride;
   int32_t part_rows;
 };
 
@@ -84,6 +84,10 @@ Layout layout_of(const hermes_config *c) {
   off = round_up(off + sizeof(uint32_t) * (size_t)s.keys_lstride * c->n_layers);
   s.kept = off;
   off = round_up(off + sizeof(int32_t) * (size_t)s.kept_lstride * c->n_layers);
+  // fp64 partials of the attention-score normaliser, one per kNormBlock candidates
+  s.normpart_lstride = (c->max_cap + kNormBlock - 1) / kNormBlock;
+  s.normpart = off;
+  off = round_up(off + sizeof(double) * (size_t)s.normpart_lstride * c->n_layers);
   s.wpart_lstride = (int64_t)c->n_kv_heads * c->max_cap;
   s.wpart = off;
   off = round_up(off + sizeof(double) * (size_t)s.wpart_lstride * c->n_layers);
@@ -496,6 +500,8 @@ static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void
   cs.wpart = reinterpret_cast<double *>(ctx->ws + ctx->lay.wpart);
   cs.wpart_lstride = ctx->lay.wpart_lstride;
   cs.wpart_hstride = ctx->max_cap;
+  cs.normpart = reinterpret_cast<double *>(ctx->ws + ctx->lay.normpart);
+  cs.normpart_lstride = ctx->lay.normpart_lstride;
   cs.q_lstride = q_ls;
   cs.kv_lstride = kv_ls;
   cs.lse_lstride = at.lse_lstride;
@@ -518,6 +524,7 @@ static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void
       cs.layer_id[n_cs] = (int8_t)l;
       cs.slot[n_cs] = slot;
       cs.cur[n_cs] = ctx->cur[l];
+      cs.alpha_mode[n_cs] = (int8_t)ctx->alpha_mode;
       max_T = ctx->len[l] + n_new > max_T ? ctx->len[l] + n_new : max_T;
       ++n_cs;
     }
@@ -599,6 +606,8 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
   cs.wpart = reinterpret_cast<double *>(ctx->ws + ctx->lay.wpart);
   cs.wpart_lstride = ctx->lay.wpart_lstride;
   cs.wpart_hstride = ctx->max_cap;
+  cs.normpart = reinterpret_cast<double *>(ctx->ws + ctx->lay.normpart);
+  cs.normpart_lstride = ctx->lay.normpart_lstride;
   cs.q_lstride = q_ls;
   cs.kv_lstride = kv_ls;
   cs.lse_lstride = at.lse_lstride;
@@ -615,6 +624,7 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
     at.layer_id[j] = cs.layer_id[j] = (int8_t)l;
     at.slot[j] = cs.slot[j] = slot;
     at.cur[j] = cs.cur[j] = ctx->cur[l];
+    cs.alpha_mode[j] = 1;   // every prompt row sees every candidate: A = W / sum W
     max_T = ctx->len[l] > max_T ? ctx->len[l] : max_T;
   }
   const int n = (int)list.size();
@@ -656,6 +666,8 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
   sa.tab = ctx->d_tab;
   sa.keys = reinterpret_cast<uint32_t *>(ctx->ws + ctx->lay.keys);
   sa.kept = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.kept);
+  sa.normpart = reinterpret_cast<const double *>(ctx->ws + ctx->lay.normpart);
+  sa.normpart_lstride = ctx->lay.normpart_lstride;
   sa.keys_lstride = ctx->lay.keys_lstride;
   sa.kept_lstride = ctx->lay.kept_lstride;
   sa.forget_rate = ctx->forget_rate;

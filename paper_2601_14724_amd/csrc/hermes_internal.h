@@ -63,7 +63,8 @@ struct ColsumArgs {
   const uint16_t *q, *kn, *vn;
   const float *lse;
   double *wpart;
-  int64_t q_lstride, kv_lstride, lse_lstride, wpart_lstride, wpart_hstride;
+  double *normpart;         // [n_layers][normpart_lstride] fp64 partials of sum_i alpha_i W_i
+  int64_t q_lstride, kv_lstride, lse_lstride, wpart_lstride, wpart_hstride, normpart_lstride;
   int32_t Hq, Hkv, C;
   float scale_log2;
   int32_t T0[kMaxLayers];
@@ -71,6 +72,7 @@ struct ColsumArgs {
   int8_t layer_id[kMaxLayers];
   int8_t slot[kMaxLayers];
   int8_t cur[kMaxLayers];
+  int8_t alpha_mode[kMaxLayers];   // weighting of the normaliser partials (0 per observer, 1 plain)
 };
 
 // Scoring, smoothing and selection; one workgroup per listed layer.  len and
@@ -79,10 +81,11 @@ struct SelectArgs {
   const LayerTable *tab;
   uint32_t *keys;           // [n_layers][max_cap]
   int32_t *kept;            // [n_layers][max_budget]
-  int64_t keys_lstride, kept_lstride;
+  const double *normpart;   // normaliser partials written with W (kNormBlock candidates each)
+  int64_t keys_lstride, kept_lstride, normpart_lstride;
   double forget_rate;
   int32_t n_layers, C, alpha_mode, align_mode;
-  int32_t n_list;
+  int32_t n_list;           // layers over budget, in layer_id
   int32_t len[kMaxLayers];
   int32_t guide_rows[kMaxLayers];   // by layer: > 0 = W came from that many prompt rows
   int8_t cur[kMaxLayers];
@@ -182,5 +185,6 @@ constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the swee
 constexpr int kSummaryRows = 512;        // candidates per workgroup of the summary sums
 constexpr int kSplitMaxTokens = 64;      // passes of at most this many rows use split keys
 constexpr int kMaxSplits = 4;
+constexpr int kNormBlock = 256;         // candidates per fp64 partial of the score normaliser
 
 }  // namespace hermes

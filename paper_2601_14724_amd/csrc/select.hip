@@ -1,17 +1,20 @@
-// Scoring, cross-layer smoothing and TopK selection for gfx950.
-//
-// One 1024-thread workgroup per layer over budget:
-//   1. importance S^l_i by class (Sec. 3.1): recency R_i = e^{-k(T-1-i)}/Z
-//      (shallow), attention A_i = alpha_i W_i normalised to sum 1 (deep), and
-//      (1 - omega_l) A + omega_l R (middle), all in fp64;
-//   2. one-hop smoothing S~^l = (1 - lambda_l) S^l + lambda_l S^{l+1}_{j(i)}
-//      (Sec. 3.2), the partner j(i) found by binary search on layer l+1's
-//      positions (or equal physical index);
-//   3. S~ rounded to fp32; its bit pattern is an order-preserving uint32 key;
-//   4. MSB-first radix select (4 passes of 8 bits, LDS histograms) finds the
-//      budget-th largest key; ties at that key go to the higher index;
-//   5. the kept indices are emitted in ascending order by two block scans.
+// Scoring, cross-layer smoothing and TopK selection for gfx950, in two
+// launches over the layers over budget:
+//   score_keys   importance S^l_i by class (Sec. 3.1): recency
+//                R_i = e^{-k(T-1-i)}/Z (shallow), attention A_i = alpha_i W_i
+//                normalised to sum 1 (deep), (1 - omega_l) A + omega_l R
+//                (middle), in fp64, A normalised by the sum of the fp64
+//                partials the mass reduction wrote with W; one-hop smoothing S~^l = (1 - lambda_l)
+//                S^l + lambda_l S^{l+1}_{j(i)} (Sec. 3.2), the partner j(i)
+//                found on layer l+1's sorted positions (or equal physical
+//                index); S~ rounded to fp32, whose bit pattern is an
+//                order-preserving uint32 key (many workgroups per layer);
+//   select_kept  MSB-first radix select (4 passes of 8 bits, LDS histograms)
+//                for the budget-th largest key, ties at that key to the
+//                higher index, the kept indices emitted in ascending order by
+//                two block scans (one workgroup per layer).
 #include "hermes_internal.h"
+#include "score_terms.h"
 
 namespace hermes {
 namespace {
@@ -29,138 +32,161 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-struct ScanShared {
-  int wsum[NW];
-  int woff[NW];
-  int total;
-};
-
-// Exclusive prefix sum over the block in thread order; *total gets the sum.
-__device__ int block_excl_scan(int v, ScanShared &sh, int *total) {
-  const int w = threadIdx.x >> 6, ln = threadIdx.x & 63;
-  const int inc = wave_incl_scan(v);
-  if (ln == 63) sh.wsum[w] = inc;
-  __syncthreads();
-  if (w == 0) {
-    const int x = ln < NW ? sh.wsum[ln] : 0;
-    const int xi = wave_incl_scan(x);
-    if (ln < NW) sh.woff[ln] = xi - x;
-    if (ln == NW - 1) sh.total = xi;
-  }
-  __syncthreads();
-  const int res = inc - v + sh.woff[w];
-  *total = sh.total;
-  __syncthreads();
-  return res;
-}
-
-__device__ double block_sum_f64(double v, double *sh) {
-  const int w = threadIdx.x >> 6, ln = threadIdx.x & 63;
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
-  if (ln == 0) sh[w] = v;
-  __syncthreads();
-  double t = 0.0;
-  for (int i = 0; i < NW; ++i) t += sh[i];   // fixed order: deterministic
-  __syncthreads();
-  return t;
-}
-
-// hist[d] += 1 for every active lane with d >= 0.  Lanes holding the same
-// digit are merged with a ballot first (the leading digits of fp32 keys are
-// shared by most candidates, so plain LDS atomics would serialise).
-__device__ __forceinline__ void hist_add(unsigned *hist, int d) {
-  const int lane = threadIdx.x & 63;
-  unsigned long long active = __ballot(d >= 0);
-  for (int it = 0; it < 3 && active != 0ull; ++it) {
-    const int leader = __ffsll(active) - 1;
-    const int dl = __shfl(d, leader);
-    const unsigned long long m = __ballot(d == dl);
-    if (lane == leader) atomicAdd(&hist[dl], (unsigned)__popcll(m));
-    active &= ~m;
-  }
-  if ((active >> lane) & 1ull) atomicAdd(&hist[d], 1u);
-}
-
 struct SelectShared {
-  unsigned hist[256];
-  int digit, above;
-  ScanShared scan;
-  double red[NW];
+  unsigned hist[2][256];      // double-buffered: the next pass's is cleared during this scan
+  int digit[2], above[2];
+  uint32_t kmin[NW], kmax[NW];
+  unsigned long long wtot[NW];
 };
 
-// Keep the M largest of keys[0..T) (M < T), ties to the higher index; write
-// the kept indices ascending to out (and out2 if non-null).
-template <typename KeyPtr>
-__device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *out, int32_t *out2,
-                                           SelectShared &sh) {
-  const int tid = threadIdx.x;
-  uint32_t prefix = 0u, pmask = 0u;
+// Block-wide min and max of the keys; on return sh.hist[0] is cleared and
+// every thread holds both.  kmin / kmax come in as this thread's own.
+__device__ __forceinline__ void block_minmax(uint32_t &kmin, uint32_t &kmax, SelectShared &sh) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    kmin = min(kmin, (uint32_t)__shfl_xor((int)kmin, o));
+    kmax = max(kmax, (uint32_t)__shfl_xor((int)kmax, o));
+  }
+  if (lane == 0) {
+    sh.kmin[wv] = kmin;
+    sh.kmax[wv] = kmax;
+  }
+  if (tid < 256) sh.hist[0][tid] = 0u;
+  __syncthreads();
+  for (int w = 0; w < NW; ++w) {
+    kmin = min(kmin, sh.kmin[w]);
+    kmax = max(kmax, sh.kmax[w]);
+  }
+}
+
+// The M-th largest of keys[0..T) (0 < M < T) by an MSB-first radix select,
+// 8 bits per pass and two barriers per pass, over the bits below the prefix
+// every key shares (the leading digits of nearby fp32 scores are nearly all
+// equal, and a histogram of equal digits serialises on one LDS address).
+// Needs block_minmax first.  *want gets how many keys equal to the result
+// are kept.  SEG: lane l reads its own segment of an odd length, so a
+// wave's 64 reads fall in 64 different places of the key array (scores are
+// correlated with their index, and neighbouring keys share digits) and in
+// distinct LDS banks; otherwise the block reads the keys with unit stride
+// (the form for keys in global memory).
+template <bool SEG, typename KeyPtr>
+__device__ __forceinline__ uint32_t radix_threshold(KeyPtr keys, int T, int M, uint32_t kmin,
+                                                    uint32_t kmax, SelectShared &sh, int *want_out) {
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int seg = ((T + 63) / 64) | 1;
+  int hi = kmin == kmax ? 0 : 32 - __clz(kmin ^ kmax);   // bits below the shared prefix
+  uint32_t pmask = hi >= 32 ? 0u : 0xffffffffu << hi;
+  uint32_t prefix = kmin & pmask;
   int want = M;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    for (int i = tid; i < 256; i += NT) sh.hist[i] = 0u;
-    if (tid == 0) {
-      sh.digit = 0;
-      sh.above = 0;
-    }
-    __syncthreads();
-    for (int i = tid; i < T; i += NT) {
-      const uint32_t k = keys[i];
-      hist_add(sh.hist, (k & pmask) == prefix ? (int)((k >> shift) & 255u) : -1);
+  for (int pass = 0; hi > 0; ++pass) {
+    const int width = min(8, hi), shift = hi - width, hb = pass & 1;
+    const uint32_t dm = (1u << width) - 1u;
+    if constexpr (SEG) {
+      for (int c = wv; c < seg; c += NW) {
+        const int i = lane * seg + c;
+        if (i < T) {
+          const uint32_t k = keys[i];
+          if ((k & pmask) == prefix) atomicAdd(&sh.hist[hb][(k >> shift) & dm], 1u);
+        }
+      }
+    } else {
+      for (int i = tid; i < T; i += NT) {
+        const uint32_t k = keys[i];
+        if ((k & pmask) == prefix) atomicAdd(&sh.hist[hb][(k >> shift) & dm], 1u);
+      }
     }
     __syncthreads();
     if (tid < 64) {
-      // lane ln owns digits 255-4ln .. 252-4ln, visited from high to low
+      // lane owns digits 255-4t .. 252-4t, visited from high to low
       int cnt[4], loc = 0;
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        cnt[e] = (int)sh.hist[255 - 4 * tid - e];
+        cnt[e] = (int)sh.hist[hb][255 - 4 * tid - e];
         loc += cnt[e];
       }
-      const int incl = wave_incl_scan(loc);
-      int acc = incl - loc;   // keys whose digit is above this lane's digits
+      int acc = wave_incl_scan(loc) - loc;   // keys whose digit is above this lane's
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (acc < want && want <= acc + cnt[e]) {
-          sh.digit = 255 - 4 * tid - e;
-          sh.above = acc;
+          sh.digit[hb] = 255 - 4 * tid - e;
+          sh.above[hb] = acc;
         }
         acc += cnt[e];
       }
+    } else if (tid < 64 + 256) {
+      sh.hist[hb ^ 1][tid - 64] = 0u;
     }
     __syncthreads();
-    want -= sh.above;
-    prefix |= (uint32_t)sh.digit << shift;
-    pmask |= 255u << shift;
-    __syncthreads();
+    want -= sh.above[hb];
+    prefix |= (uint32_t)sh.digit[hb] << shift;
+    pmask |= dm << shift;
+    hi = shift;
   }
-  const uint32_t thr = prefix;   // the M-th largest key; `want` ties of it are kept
+  *want_out = want;
+  return prefix;
+}
 
+// Output place of a contiguous run holding gt keys above the threshold and
+// eq equal to it, when the `want` equal keys of highest index are kept: one
+// block scan of the packed (gt, eq) pair.  *skip gets how many of the run's
+// equal keys (its first ones) are dropped.
+__device__ __forceinline__ int kept_offset(unsigned gt, unsigned eq, int want, SelectShared &sh, int *skip) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const unsigned long long mine = ((unsigned long long)gt << 32) | eq;
+  unsigned long long inc = mine;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const unsigned long long x = __shfl_up(inc, o);
+    if (lane >= o) inc += x;
+  }
+  if (lane == 63) sh.wtot[wv] = inc;
+  __syncthreads();
+  unsigned long long before = inc - mine, total = 0;
+  for (int w = 0; w < NW; ++w) {
+    const unsigned long long x = sh.wtot[w];
+    before += w < wv ? x : 0ull;
+    total += x;
+  }
+  const int eq_total = (int)(uint32_t)total;
+  const int eq_before = (int)(uint32_t)before, gt_before = (int)(before >> 32);
+  const int drop = eq_total - want;   // ties dropped: those of lowest index
+  *skip = min((int)eq, max(0, drop - eq_before));
+  return gt_before + max(0, eq_before - drop);
+}
+
+// Keep the M largest of keys[0..T) (M < T), ties to the higher index; write
+// the kept indices ascending to out (and out2 if non-null).  Thread t owns
+// the contiguous run [a0, a1) for the output.
+template <bool SEG, typename KeyPtr>
+__device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *out, int32_t *out2,
+                                           SelectShared &sh) {
+  const int tid = threadIdx.x;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  for (int i = tid; i < T; i += NT) {
+    const uint32_t k = keys[i];
+    kmin = min(kmin, k);
+    kmax = max(kmax, k);
+  }
+  block_minmax(kmin, kmax, sh);
+  int want;
+  const uint32_t thr = radix_threshold<SEG>(keys, T, M, kmin, kmax, sh, &want);
   const int per = (T + NT - 1) / NT;
   const int a0 = min(T, tid * per), a1 = min(T, a0 + per);
-  int gt = 0, eq = 0;
+  unsigned gt = 0, eq = 0;
   for (int i = a0; i < a1; ++i) {
     const uint32_t k = keys[i];
     gt += k > thr;
     eq += k == thr;
   }
-  int eq_total;
-  const int eq_before = block_excl_scan(eq, sh.scan, &eq_total);
-  const int eq_above = eq_total - eq_before - eq;        // ties at higher indices
-  const int keep_eq = max(0, min(eq, want - eq_above));  // my highest keep_eq ties stay
-  int kept_total;
-  int off = block_excl_scan(gt + keep_eq, sh.scan, &kept_total);
-  int skip = eq - keep_eq;
+  int skip;
+  int off = kept_offset(gt, eq, want, sh, &skip);
   for (int i = a0; i < a1; ++i) {
     const uint32_t k = keys[i];
     bool keep = k > thr;
     if (k == thr) {
-      if (skip > 0) {
-        --skip;
-      } else {
-        keep = true;
-      }
+      if (skip > 0) --skip;
+      else keep = true;
     }
     if (keep && off < M) {   // off < M always holds; the guard keeps writes in bounds
       out[off] = i;
@@ -170,44 +196,115 @@ __device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *o
   }
 }
 
-__device__ __forceinline__ double mass_over_observers(float w, int i, int T0, int C, int mode) {
-  if (mode != 0) return (double)w;
-  const int n = i < T0 ? C : C - (i - T0);
-  return (double)w / (double)n;
-}
-
 __device__ __forceinline__ double class_score(int cls, double om, double a, double r) {
   if (cls == HERMES_SHALLOW) return r;
   if (cls == HERMES_DEEP) return a;
   return (1.0 - om) * a + om * r;
 }
 
-// Candidates whose positions / keys fit in LDS take the LDS path; longer
-// layers fall back to global memory (L2-resident) with the same arithmetic.
+// Keys of layers with at most this many candidates are staged in LDS for the
+// select passes; longer layers read them from global memory (L2-resident).
 constexpr int kLdsKeys = 38400;   // 150 KiB
+// Positions of the layer above with at most this many candidates are staged
+// in LDS for the partner search.
+constexpr int kLdsPos = 12288;    // 48 KiB
 
-// Index of `target` in the sorted array p[0..n), or -1.
-template <typename Ptr>
-__device__ __forceinline__ int find_sorted(Ptr p, int n, int target, int hint) {
-  if (hint < n && p[hint] == target) return hint;   // same physical index
-  int lo = 0, hi = n - 1;
-  while (lo <= hi) {
-    const int mid = (lo + hi) >> 1;
-    const int v = p[mid];
-    if (v == target) return mid;
-    if (v < target) lo = mid + 1; else hi = mid - 1;
+// dst[0..n) = src[0..n) for a 4-byte aligned src, by the NTHR threads of the
+// block: the elements before the first 16-byte boundary one by one, then
+// 16-byte loads, R per thread issued before any is stored so their latencies
+// overlap, then the last < 4 elements.  The caller synchronises.
+template <int NTHR, int R>
+__device__ __forceinline__ void stage_u32(const uint32_t *src, int n, uint32_t *dst) {
+  const int tid = threadIdx.x;
+  const int head = min(n, (int)(((16u - (uint32_t)(reinterpret_cast<uintptr_t>(src) & 15u)) & 15u) >> 2));
+  if (tid < head) dst[tid] = src[tid];
+  const int nv = (n - head) >> 2;
+  const uint4 *s4 = reinterpret_cast<const uint4 *>(src + head);
+  for (int b = 0; b < nv; b += NTHR * R) {
+    uint4 r[R];
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int q = b + u * NTHR + tid;
+      if (q < nv) r[u] = s4[q];
+    }
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int q = b + u * NTHR + tid;
+      if (q < nv) {
+        uint32_t *d = dst + head + 4 * q;
+        d[0] = r[u].x;
+        d[1] = r[u].y;
+        d[2] = r[u].z;
+        d[3] = r[u].w;
+      }
+    }
   }
-  return -1;
+  const int t0 = head + 4 * nv;
+  if (t0 + tid < n) dst[t0 + tid] = src[t0 + tid];
 }
 
-__global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
-  __shared__ SelectShared sh;
-  __shared__ uint32_t big[kLdsKeys];
-  const int tid = threadIdx.x;
-  const int l = a.layer_id[blockIdx.x];
+// Normaliser of the attention score (Sec. 3.1): the fixed-order sum of the
+// layer's per-block partials of alpha_i W_i (written with W), over the n
+// blocks covering its T candidates.  Every wave computes it alone (lane b
+// sums partials b, b+64, ... in order, then a fixed butterfly), so every
+// wave of every workgroup gets the same bits.
+__device__ __forceinline__ double sum_partials(const double *p, int n) {
+  const int lane = threadIdx.x & 63;
+  double s = 0.0;
+  for (int b = lane; b < n; b += 64) s += p[b];
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  return s;
+}
+
+// First index in [lo, n) of the sorted p with p[idx] >= x: a few linear
+// steps (partners of consecutive candidates are usually adjacent), then a
+// binary search.
+template <typename Ptr>
+__device__ __forceinline__ int lower_bound_from(Ptr p, int lo, int n, int x) {
+#pragma unroll
+  for (int s = 0; s < 4; ++s) {
+    if (lo >= n || p[lo] >= x) return lo;
+    ++lo;
+  }
+  int hi = n;
+  while (lo < hi) {
+    const int mid = (lo + hi) >> 1;
+    if (p[mid] < x) lo = mid + 1;
+    else hi = mid;
+  }
+  return lo;
+}
+
+// Partners j(i) in the layer above of KU consecutive candidates with
+// positions pv (ascending): one search for the first, a forward walk after.
+template <int KU, typename Ptr>
+__device__ __forceinline__ void partners(Ptr p1, int T1, const int *pv, int i0, int T, int *jx) {
+  int lb = 0;
+#pragma unroll
+  for (int u = 0; u < KU; ++u) {
+    if (i0 + u >= T) {
+      jx[u] = -1;
+      continue;
+    }
+    lb = lower_bound_from(p1, lb, T1, pv[u]);
+    jx[u] = (lb < T1 && p1[lb] == pv[u]) ? lb : -1;
+  }
+}
+
+// 1. Smoothed keys of every candidate of the listed layers (Sec. 3.1 scores,
+//    Sec. 3.2 smoothing), KU consecutive candidates per thread, with the
+//    positions of the layer above staged in LDS for the partner search.
+constexpr int KT = 256;
+constexpr int KU = 4;
+__global__ __launch_bounds__(KT) void score_keys(SelectArgs a) {
+  __shared__ int32_t spos[kLdsPos];
+  const int l = a.layer_id[blockIdx.y];
   const LayerTable &L0 = a.tab[l];
   const int C = a.C;
   const int T = a.len[l];
+  const int i0 = (blockIdx.x * KT + threadIdx.x) * KU;
+  if (blockIdx.x * KT * KU >= T) return;   // whole block past the layer's end
   const int T0 = T - C;
   const int32_t *pos = L0.pos[a.cur[l]];
   const float *w = L0.w;
@@ -216,7 +313,6 @@ __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
   const double lam = L0.lambda;
   const double k = a.forget_rate;
   const bool has_next = (l + 1 < a.n_layers) && lam != 0.0;
-
   int T1 = 0, T01 = 0, cls1 = HERMES_SHALLOW;
   const int32_t *pos1 = nullptr;
   const float *w1 = nullptr;
@@ -230,89 +326,315 @@ __global__ __launch_bounds__(NT) void score_select(SelectArgs a) {
     cls1 = L1.cls;
     om1 = L1.omega;
   }
-  // W from a guidance prompt: every candidate has the same observers, so the
-  // normalised mass is W / sum W whatever alpha_mode says.
   const int am0 = a.guide_rows[l] > 0 ? 1 : a.alpha_mode;
   const int am1 = (has_next && a.guide_rows[l + 1] > 0) ? 1 : a.alpha_mode;
   const bool needA0 = cls != HERMES_SHALLOW, needR0 = cls != HERMES_DEEP;
   const bool needA1 = has_next && cls1 != HERMES_SHALLOW;
   const bool needR1 = has_next && cls1 != HERMES_DEEP;
-  const bool lds = T <= kLdsKeys && T1 <= kLdsKeys;
   const bool by_pos = has_next && a.align_mode == 0;
+  const bool pos_lds = by_pos && T1 <= kLdsPos;
 
-  // Normalisers: the alpha-weighted mass summed in a fixed order, and the
-  // recency curve's closed-form sum Z = (1 - e^{-kT}) / (1 - e^{-k}).
-  double sa0 = 0.0, sa1 = 0.0;
-  if (needA0)
-    for (int i = tid; i < T; i += NT) sa0 += mass_over_observers(w[i], i, T0, C, am0);
-  if (needA1)
-    for (int i = tid; i < T1; i += NT) sa1 += mass_over_observers(w1[i], i, T01, C, am1);
-  if (lds && by_pos)
-    for (int i = tid; i < T1; i += NT) big[i] = (uint32_t)pos1[i];
-  sa0 = block_sum_f64(sa0, sh.red);
-  sa1 = block_sum_f64(sa1, sh.red);
+  int pv[KU], jx[KU];
+  float wv[KU], w1v[KU];
+#pragma unroll
+  for (int u = 0; u < KU; ++u) {
+    const int i = i0 + u;
+    const bool ok = i < T;
+    wv[u] = (ok && needA0) ? w[i] : 0.f;
+    pv[u] = (ok && by_pos) ? pos[i] : 0;
+  }
+  // every lane of the wave takes part in the butterfly: before any lane exits
+  const int nb0 = (T + kNormBlock - 1) / kNormBlock, nb1 = (T1 + kNormBlock - 1) / kNormBlock;
+  const double sa0 = needA0 ? sum_partials(a.normpart + l * a.normpart_lstride, nb0) : 0.0;
+  const double sa1 = needA1 ? sum_partials(a.normpart + (l + 1) * a.normpart_lstride, nb1) : 0.0;
+  if (pos_lds) {   // uniform over the block
+    stage_u32<KT, 12>(reinterpret_cast<const uint32_t *>(pos1), T1, reinterpret_cast<uint32_t *>(spos));
+    __syncthreads();
+  }
+  if (i0 >= T) return;
+  if (by_pos) {
+    if (pos_lds) partners<KU>(static_cast<const int32_t *>(spos), T1, pv, i0, T, jx);
+    else partners<KU>(pos1, T1, pv, i0, T, jx);
+  } else {
+#pragma unroll
+    for (int u = 0; u < KU; ++u) jx[u] = (has_next && i0 + u < T && i0 + u < T1) ? i0 + u : -1;
+  }
+#pragma unroll
+  for (int u = 0; u < KU; ++u) w1v[u] = (jx[u] >= 0 && needA1) ? w1[jx[u]] : 0.f;
+
+  const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
+  // recency normaliser in closed form: Z = (1 - e^{-kT}) / (1 - e^{-k})
   const double z0 = expm1(-k * (double)T) / expm1(-k);
   const double z1 = expm1(-k * (double)T1) / expm1(-k);
-
-  uint32_t *keys = a.keys + l * a.keys_lstride;
-  const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
   const double inv_z0 = 1.0 / z0, inv_z1 = T1 > 0 ? 1.0 / z1 : 0.0;
-  constexpr int U = 4;   // candidates per thread per pass: their loads are in flight together
-  for (int i0 = tid; i0 < T; i0 += U * NT) {
-    int ii[U], pv[U], jx[U];
-    float wv[U], w1v[U];
+  uint32_t *keys = a.keys + l * a.keys_lstride;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      ii[u] = i0 + u * NT;
-      const bool ok = ii[u] < T;
-      wv[u] = (ok && needA0) ? w[ii[u]] : 0.f;
-      pv[u] = (ok && by_pos) ? pos[ii[u]] : 0;
-    }
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      jx[u] = -1;
-      if (ii[u] < T && has_next) {
-        if (by_pos) {
-          jx[u] = lds ? find_sorted(reinterpret_cast<const int32_t *>(big), T1, pv[u], ii[u])
-                      : find_sorted(pos1, T1, pv[u], ii[u]);
-        } else {
-          jx[u] = ii[u] < T1 ? ii[u] : -1;
-        }
+  for (int u = 0; u < KU; ++u) {
+    const int i = i0 + u;
+    if (i >= T) break;
+    const double a_i = needA0 ? mass_over_observers(wv[u], i, T0, C, am0) * inv_sa0 : 0.0;
+    const double r_i = needR0 ? exp(-k * (double)(T - 1 - i)) * inv_z0 : 0.0;
+    double st = class_score(cls, om, a_i, r_i);
+    if (has_next) {
+      double s1 = 0.0;
+      const int j = jx[u];
+      if (j >= 0) {
+        const double a_j = needA1 ? mass_over_observers(w1v[u], j, T01, C, am1) * inv_sa1 : 0.0;
+        const double r_j = needR1 ? exp(-k * (double)(T1 - 1 - j)) * inv_z1 : 0.0;
+        s1 = class_score(cls1, om1, a_j, r_j);
       }
+      st = (1.0 - lam) * st + lam * s1;
     }
+    const float f = (float)st;
+    keys[i] = __builtin_bit_cast(uint32_t, f);
+    if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
+  }
+}
+
+// A thread's share of one array copied to LDS by the whole block in one
+// batch: the elements before src's first 16-byte boundary one by one, up to
+// R 16-byte pieces, and the last < 4 elements.  stage_issue only loads, so
+// several arrays' loads can be in flight before any is stored.
+template <int R>
+struct Staged {
+  uint4 r[R];
+  uint32_t h, t;
+};
+
+__device__ __forceinline__ int stage_head(const uint32_t *src, int n) {
+  return min(n, (int)(((16u - (uint32_t)(reinterpret_cast<uintptr_t>(src) & 15u)) & 15u) >> 2));
+}
+
+template <int R>
+__device__ __forceinline__ void stage_issue(const uint32_t *src, int n, Staged<R> &s) {
+  const int tid = threadIdx.x;
+  const int head = stage_head(src, n);
+  const int nv = (n - head) >> 2;   // <= NT * R: one batch
+  const uint4 *s4 = reinterpret_cast<const uint4 *>(src + head);
 #pragma unroll
-    for (int u = 0; u < U; ++u) w1v[u] = (jx[u] >= 0 && needA1) ? w1[jx[u]] : 0.f;
+  for (int u = 0; u < R; ++u) {
+    const int q = u * NT + tid;
+    if (q < nv) s.r[u] = s4[q];
+  }
+  if (tid < head) s.h = src[tid];
+  const int t0 = head + 4 * nv;
+  if (t0 + tid < n) s.t = src[t0 + tid];
+}
+
+template <int R>
+__device__ __forceinline__ void stage_commit(const uint32_t *src, int n, const Staged<R> &s, uint32_t *dst) {
+  const int tid = threadIdx.x;
+  const int head = stage_head(src, n);
+  const int nv = (n - head) >> 2;
 #pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int i = ii[u];
-      if (i >= T) continue;
-      const double a_i = needA0 ? mass_over_observers(wv[u], i, T0, C, am0) * inv_sa0 : 0.0;
-      const double r_i = needR0 ? exp(-k * (double)(T - 1 - i)) * inv_z0 : 0.0;
-      double st = class_score(cls, om, a_i, r_i);
-      if (has_next) {
-        double s1 = 0.0;
-        const int j = jx[u];
-        if (j >= 0) {
-          const double a_j = needA1 ? mass_over_observers(w1v[u], j, T01, C, am1) * inv_sa1 : 0.0;
-          const double r_j = needR1 ? exp(-k * (double)(T1 - 1 - j)) * inv_z1 : 0.0;
-          s1 = class_score(cls1, om1, a_j, r_j);
-        }
-        st = (1.0 - lam) * st + lam * s1;
-      }
-      const float f = (float)st;
-      keys[i] = __builtin_bit_cast(uint32_t, f);
-      if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
+  for (int u = 0; u < R; ++u) {
+    const int q = u * NT + tid;
+    if (q < nv) {
+      uint32_t *d = dst + head + 4 * q;
+      d[0] = s.r[u].x;
+      d[1] = s.r[u].y;
+      d[2] = s.r[u].z;
+      d[3] = s.r[u].w;
     }
   }
-  __syncthreads();
-  if (T <= L0.budget) return;
-  int32_t *kept = a.kept + l * a.kept_lstride;
-  if (lds) {
-    for (int i = tid; i < T; i += NT) big[i] = keys[i];
-    __syncthreads();
-    select_top(big, T, L0.budget, kept, L0.kept_dbg, sh);
+  if (tid < head) dst[tid] = s.h;
+  const int t0 = head + 4 * nv;
+  if (t0 + tid < n) dst[t0 + tid] = s.t;
+}
+
+// e^{-k (Tm1 - j)} for increasing j: from the previous value by factors of
+// e^{k} when the gap is short (a few fp64 ulps from the direct form), else
+// directly.
+__device__ __forceinline__ double recency_next(double &val, int &jprev, int j, double k, double ek, int Tm1) {
+  const int gap = j - jprev;
+  if (jprev >= 0 && gap <= 4) {
+    for (int g = 0; g < gap; ++g) val *= ek;
   } else {
-    select_top(keys, T, L0.budget, kept, L0.kept_dbg, sh);
+    val = exp(-k * (double)(Tm1 - j));
+  }
+  jprev = j;
+  return val;
+}
+
+// alpha_i W_i with the cached rows' 1/C as a product (a division only for
+// the chunk's own rows).
+__device__ __forceinline__ double mass_scaled(float w, int i, int T0, int C, int mode, double inv_c) {
+  if (mode != 0) return (double)w;
+  if (i < T0) return (double)w * inv_c;
+  return (double)w / (double)(C - (i - T0));
+}
+
+// Scores, smoothing and TopK of one layer in one workgroup (layers of at
+// most kFusedT candidates whose layer above has at most kFusedT): the same
+// quantities as score_keys + select_kept without the keys' round trip
+// through global memory and the second launch.
+//   1. W and positions of layers l and l+1 staged in LDS by coalesced
+//      16-byte loads, all issued before any is stored; the normalisers from
+//      the partials written with W;
+//   2. thread t scores the contiguous run of at most FR candidates it owns
+//      (the partner found from the same index or by a forward search in
+//      LDS, recency by factors of e^{k}), keys kept in registers;
+//   3. the keys go to LDS for the radix passes, then the run's kept indices
+//      go out from the registers.
+constexpr int kFusedT = 9216;
+constexpr int FR = kFusedT / NT;
+
+__global__ __launch_bounds__(NT) void select_fused(SelectArgs a) {
+  __shared__ __align__(16) uint32_t s_w[kFusedT];     // W of layer l as bits, then the keys
+  __shared__ __align__(16) int32_t s_pos[kFusedT];    // positions of layer l
+  __shared__ __align__(16) int32_t s_pos1[kFusedT];   // positions of layer l+1
+  __shared__ __align__(16) uint32_t s_w1[kFusedT];    // W of layer l+1 as bits
+  __shared__ SelectShared sh;
+  const int tid = threadIdx.x;
+  const int l = a.layer_id[blockIdx.x];
+  const LayerTable &L0 = a.tab[l];
+  const int C = a.C;
+  const int T = a.len[l];
+  const int M = L0.budget;
+  const int T0 = T - C;
+  const int32_t *pos = L0.pos[a.cur[l]];
+  const int cls = L0.cls;
+  const double om = L0.omega, lam = L0.lambda, k = a.forget_rate;
+  const bool has_next = (l + 1 < a.n_layers) && lam != 0.0;
+  int T1 = 0, T01 = 0, cls1 = HERMES_SHALLOW;
+  const int32_t *pos1 = nullptr;
+  const float *w1 = nullptr;
+  double om1 = 0.0;
+  if (has_next) {
+    const LayerTable &L1 = a.tab[l + 1];
+    T1 = a.len[l + 1];
+    T01 = T1 - C;
+    pos1 = L1.pos[a.cur[l + 1]];
+    w1 = L1.w;
+    cls1 = L1.cls;
+    om1 = L1.omega;
+  }
+  const int am0 = a.guide_rows[l] > 0 ? 1 : a.alpha_mode;
+  const int am1 = (has_next && a.guide_rows[l + 1] > 0) ? 1 : a.alpha_mode;
+  const bool needA0 = cls != HERMES_SHALLOW, needR0 = cls != HERMES_DEEP;
+  const bool needA1 = has_next && cls1 != HERMES_SHALLOW;
+  const bool needR1 = has_next && cls1 != HERMES_DEEP;
+  const bool by_pos = has_next && a.align_mode == 0;
+
+  // 1. staging (every condition is uniform over the block)
+  {
+    Staged<3> g0, g1, g2, g3;
+    if (needA0) stage_issue(reinterpret_cast<const uint32_t *>(L0.w), T, g0);
+    if (by_pos) {
+      stage_issue(reinterpret_cast<const uint32_t *>(pos), T, g1);
+      stage_issue(reinterpret_cast<const uint32_t *>(pos1), T1, g2);
+    }
+    if (needA1) stage_issue(reinterpret_cast<const uint32_t *>(w1), T1, g3);
+    if (needA0) stage_commit(reinterpret_cast<const uint32_t *>(L0.w), T, g0, s_w);
+    if (by_pos) {
+      stage_commit(reinterpret_cast<const uint32_t *>(pos), T, g1, reinterpret_cast<uint32_t *>(s_pos));
+      stage_commit(reinterpret_cast<const uint32_t *>(pos1), T1, g2, reinterpret_cast<uint32_t *>(s_pos1));
+    }
+    if (needA1) stage_commit(reinterpret_cast<const uint32_t *>(w1), T1, g3, s_w1);
+  }
+  const int nb0 = (T + kNormBlock - 1) / kNormBlock, nb1 = (T1 + kNormBlock - 1) / kNormBlock;
+  const double sa0 = needA0 ? sum_partials(a.normpart + l * a.normpart_lstride, nb0) : 0.0;
+  const double sa1 = needA1 ? sum_partials(a.normpart + (l + 1) * a.normpart_lstride, nb1) : 0.0;
+  __syncthreads();
+
+  // 2. keys of this thread's run
+  const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
+  const double z0 = expm1(-k * (double)T) / expm1(-k);
+  const double z1 = expm1(-k * (double)T1) / expm1(-k);
+  const double inv_z0 = 1.0 / z0, inv_z1 = T1 > 0 ? 1.0 / z1 : 0.0;
+  const double ek = exp(k), inv_c = 1.0 / (double)C;
+  const float *s_wf = reinterpret_cast<const float *>(s_w);
+  const float *s_w1f = reinterpret_cast<const float *>(s_w1);
+  const int per = (T + NT - 1) / NT;
+  const int b0 = min(T, tid * per), e0 = min(T, b0 + per);
+  uint32_t kr[FR];
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+  int lb = 0, jp0 = -1, jp1 = -1;
+  double rv0 = 0.0, rv1 = 0.0;
+#pragma unroll
+  for (int u = 0; u < FR; ++u) {
+    const int i = b0 + u;
+    kr[u] = 0u;
+    if (i >= e0) continue;
+    const double a_i = needA0 ? mass_scaled(s_wf[i], i, T0, C, am0, inv_c) * inv_sa0 : 0.0;
+    const double r_i = needR0 ? recency_next(rv0, jp0, i, k, ek, T - 1) * inv_z0 : 0.0;
+    double st = class_score(cls, om, a_i, r_i);
+    if (has_next) {
+      int j = -1;
+      if (by_pos) {
+        const int p = s_pos[i];
+        if (u == 0 && i < T1 && s_pos1[i] == p) lb = i;   // same physical index
+        else lb = lower_bound_from(static_cast<const int32_t *>(s_pos1), lb, T1, p);
+        j = (lb < T1 && s_pos1[lb] == p) ? lb : -1;
+      } else {
+        j = i < T1 ? i : -1;
+      }
+      double sj = 0.0;
+      if (j >= 0) {
+        const double a_j = needA1 ? mass_scaled(s_w1f[j], j, T01, C, am1, inv_c) * inv_sa1 : 0.0;
+        const double r_j = needR1 ? recency_next(rv1, jp1, j, k, ek, T1 - 1) * inv_z1 : 0.0;
+        sj = class_score(cls1, om1, a_j, r_j);
+      }
+      st = (1.0 - lam) * st + lam * sj;
+    }
+    const float f = (float)st;
+    kr[u] = __builtin_bit_cast(uint32_t, f);
+    kmin = min(kmin, kr[u]);
+    kmax = max(kmax, kr[u]);
+    if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
+  }
+  __syncthreads();   // every read of the staged W is done: s_w takes the keys
+#pragma unroll
+  for (int u = 0; u < FR; ++u)
+    if (b0 + u < e0) s_w[b0 + u] = kr[u];
+  block_minmax(kmin, kmax, sh);   // its barrier also publishes the keys
+
+  // 3. threshold, then the run's kept indices from the registers
+  int want;
+  const uint32_t thr = radix_threshold<true>(static_cast<const uint32_t *>(s_w), T, M, kmin, kmax, sh, &want);
+  unsigned gt = 0, eq = 0;
+#pragma unroll
+  for (int u = 0; u < FR; ++u)
+    if (b0 + u < e0) {
+      gt += kr[u] > thr;
+      eq += kr[u] == thr;
+    }
+  int skip;
+  int off = kept_offset(gt, eq, want, sh, &skip);
+  int32_t *kept = a.kept + l * a.kept_lstride;
+#pragma unroll
+  for (int u = 0; u < FR; ++u) {
+    const int i = b0 + u;
+    if (i >= e0) break;
+    bool keep = kr[u] > thr;
+    if (kr[u] == thr) {
+      if (skip > 0) --skip;
+      else keep = true;
+    }
+    if (keep && off < M) {   // off < M always holds; the guard keeps writes in bounds
+      kept[off] = i;
+      if (L0.kept_dbg != nullptr) L0.kept_dbg[off] = i;
+      ++off;
+    }
+  }
+}
+
+// 2. TopK of each listed layer from its keys (staged in LDS when they fit).
+__global__ __launch_bounds__(NT) void select_kept(SelectArgs a) {
+  __shared__ SelectShared sh;
+  __shared__ uint32_t big[kLdsKeys];
+  const int l = a.layer_id[blockIdx.x];
+  const LayerTable &L0 = a.tab[l];
+  const int T = a.len[l];
+  if (T <= L0.budget) return;
+  const uint32_t *keys = a.keys + l * a.keys_lstride;
+  int32_t *kept = a.kept + l * a.kept_lstride;
+  if (T <= kLdsKeys) {
+    stage_u32<NT, 10>(keys, T, big);
+    __syncthreads();
+    select_top<true>(big, T, L0.budget, kept, L0.kept_dbg, sh);
+  } else {
+    select_top<false>(keys, T, L0.budget, kept, L0.kept_dbg, sh);
   }
 }
 
@@ -322,13 +644,27 @@ __global__ __launch_bounds__(NT) void topk_keys(const uint32_t *keys, int n, int
     for (int i = threadIdx.x; i < n; i += NT) out[i] = i;
     return;
   }
-  select_top(keys, n, k, out, nullptr, sh);
+  select_top<false>(keys, n, k, out, nullptr, sh);
 }
 
 }  // namespace
 
 hipError_t launch_select(const SelectArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(score_select, dim3(a.n_list), dim3(NT), 0, s, a);
+  bool fused = true;
+  for (int j = 0; j < a.n_list; ++j) {
+    const int l = a.layer_id[j];
+    fused = fused && a.len[l] <= kFusedT && (l + 1 >= a.n_layers || a.len[l + 1] <= kFusedT);
+  }
+  if (fused) {
+    hipLaunchKernelGGL(select_fused, dim3(a.n_list), dim3(NT), 0, s, a);
+    return hipGetLastError();
+  }
+  int max_T = 0;
+  for (int j = 0; j < a.n_list; ++j) max_T = max(max_T, a.len[a.layer_id[j]]);
+  hipLaunchKernelGGL(score_keys, dim3((max_T + KT * KU - 1) / (KT * KU), a.n_list), dim3(KT), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(select_kept, dim3(a.n_list), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
