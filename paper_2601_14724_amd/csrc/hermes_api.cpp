@@ -673,6 +673,8 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
   sa.forget_rate = ctx->forget_rate;
   sa.n_layers = L;
   sa.C = ctx->step_n_new;
+  sa.ek = std::exp(ctx->forget_rate);
+  sa.inv_c = 1.0 / (double)(sa.C > 0 ? sa.C : 1);
   sa.alpha_mode = ctx->alpha_mode;
   sa.align_mode = ctx->align_mode;
   GatherArgs ga;
@@ -690,6 +692,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
     sa.len[l] = ctx->len[l];
     sa.cur[l] = ctx->cur[l];
     sa.guide_rows[l] = ctx->scoring_mode == HERMES_SCORE_GUIDANCE ? ctx->guided[l] : 0;
+    sa.inv_z[l] = 1.0 / (std::expm1(-ctx->forget_rate * (double)ctx->len[l]) / std::expm1(-ctx->forget_rate));
     if (evicts(l)) {
       has_sum[l] = ctx->summary_mode && ctx->cls[l] == HERMES_DEEP;
       sa.layer_id[n] = (int8_t)l;

@@ -88,6 +88,9 @@ struct SelectArgs {
   int32_t n_list;           // layers over budget, in layer_id
   int32_t len[kMaxLayers];
   int32_t guide_rows[kMaxLayers];   // by layer: > 0 = W came from that many prompt rows
+  double inv_z[kMaxLayers];   // by layer: 1 / Z, Z = sum_{i<len} e^{-k i} = (1 - e^{-k len}) / (1 - e^{-k})
+  double ek;                  // e^{k}
+  double inv_c;               // 1 / C
   int8_t cur[kMaxLayers];
   int8_t layer_id[kMaxLayers];
 };

@@ -3,16 +3,18 @@
 //   score_keys   importance S^l_i by class (Sec. 3.1): recency
 //                R_i = e^{-k(T-1-i)}/Z (shallow), attention A_i = alpha_i W_i
 //                normalised to sum 1 (deep), (1 - omega_l) A + omega_l R
-//                (middle), in fp64, A normalised by the sum of the fp64
-//                partials the mass reduction wrote with W; one-hop smoothing S~^l = (1 - lambda_l)
-//                S^l + lambda_l S^{l+1}_{j(i)} (Sec. 3.2), the partner j(i)
-//                found on layer l+1's sorted positions (or equal physical
-//                index); S~ rounded to fp32, whose bit pattern is an
-//                order-preserving uint32 key (many workgroups per layer);
-//   select_kept  MSB-first radix select (4 passes of 8 bits, LDS histograms)
-//                for the budget-th largest key, ties at that key to the
-//                higher index, the kept indices emitted in ascending order by
-//                two block scans (one workgroup per layer).
+//                (middle), in fp64, the normaliser of A summed from the fp64
+//                partials the mass reduction wrote with W; one-hop smoothing
+//                S~^l = (1 - lambda_l) S^l + lambda_l S^{l+1}_{j(i)}
+//                (Sec. 3.2), the partner j(i) found on layer l+1's sorted
+//                positions (or at the equal physical index); S~ rounded to
+//                fp32, whose bit pattern is an order-preserving uint32 key
+//                (several workgroups per layer);
+//   select_kept  the budget-th largest key by an MSB-first radix select over
+//                the bits below the prefix all keys share (LDS histograms,
+//                keys in registers), ties at that key to the higher index,
+//                the kept indices emitted in ascending order from one block
+//                scan (one workgroup per layer).
 #include "hermes_internal.h"
 #include "score_terms.h"
 
@@ -60,21 +62,17 @@ __device__ __forceinline__ void block_minmax(uint32_t &kmin, uint32_t &kmax, Sel
   }
 }
 
-// The M-th largest of keys[0..T) (0 < M < T) by an MSB-first radix select,
-// 8 bits per pass and two barriers per pass, over the bits below the prefix
-// every key shares (the leading digits of nearby fp32 scores are nearly all
-// equal, and a histogram of equal digits serialises on one LDS address).
-// Needs block_minmax first.  *want gets how many keys equal to the result
-// are kept.  SEG: lane l reads its own segment of an odd length, so a
-// wave's 64 reads fall in 64 different places of the key array (scores are
-// correlated with their index, and neighbouring keys share digits) and in
-// distinct LDS banks; otherwise the block reads the keys with unit stride
-// (the form for keys in global memory).
-template <bool SEG, typename KeyPtr>
-__device__ __forceinline__ uint32_t radix_threshold(KeyPtr keys, int T, int M, uint32_t kmin,
-                                                    uint32_t kmax, SelectShared &sh, int *want_out) {
-  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  const int seg = ((T + 63) / 64) | 1;
+// The M-th largest key (0 < M < number of keys) by an MSB-first radix
+// select, 8 bits per pass and two barriers per pass, over the bits below
+// the prefix every key shares (the leading digits of nearby fp32 scores are
+// nearly all equal, and a histogram of equal digits serialises on one LDS
+// address).  Needs block_minmax first.  hist(h, pmask, prefix, shift, dm)
+// adds this thread's keys k with (k & pmask) == prefix to h[(k >> shift) &
+// dm].  *want gets how many keys equal to the result are kept.
+template <typename Hist>
+__device__ __forceinline__ uint32_t radix_select(int M, uint32_t kmin, uint32_t kmax, SelectShared &sh,
+                                                 int *want_out, Hist hist) {
+  const int tid = threadIdx.x;
   int hi = kmin == kmax ? 0 : 32 - __clz(kmin ^ kmax);   // bits below the shared prefix
   uint32_t pmask = hi >= 32 ? 0u : 0xffffffffu << hi;
   uint32_t prefix = kmin & pmask;
@@ -82,20 +80,7 @@ __device__ __forceinline__ uint32_t radix_threshold(KeyPtr keys, int T, int M, u
   for (int pass = 0; hi > 0; ++pass) {
     const int width = min(8, hi), shift = hi - width, hb = pass & 1;
     const uint32_t dm = (1u << width) - 1u;
-    if constexpr (SEG) {
-      for (int c = wv; c < seg; c += NW) {
-        const int i = lane * seg + c;
-        if (i < T) {
-          const uint32_t k = keys[i];
-          if ((k & pmask) == prefix) atomicAdd(&sh.hist[hb][(k >> shift) & dm], 1u);
-        }
-      }
-    } else {
-      for (int i = tid; i < T; i += NT) {
-        const uint32_t k = keys[i];
-        if ((k & pmask) == prefix) atomicAdd(&sh.hist[hb][(k >> shift) & dm], 1u);
-      }
-    }
+    hist(sh.hist[hb], pmask, prefix, shift, dm);
     __syncthreads();
     if (tid < 64) {
       // lane owns digits 255-4t .. 252-4t, visited from high to low
@@ -127,6 +112,51 @@ __device__ __forceinline__ uint32_t radix_threshold(KeyPtr keys, int T, int M, u
   return prefix;
 }
 
+// Radix select over keys[0..T) read from memory with unit stride.
+template <typename KeyPtr>
+__device__ __forceinline__ uint32_t radix_threshold(KeyPtr keys, int T, int M, uint32_t kmin, uint32_t kmax,
+                                                    SelectShared &sh, int *want_out) {
+  return radix_select(M, kmin, kmax, sh, want_out,
+                      [&](unsigned *h, uint32_t pmask, uint32_t prefix, int shift, uint32_t dm) {
+                        for (int i = threadIdx.x; i < T; i += NT) {
+                          const uint32_t k = keys[i];
+                          if ((k & pmask) == prefix) atomicAdd(&h[(k >> shift) & dm], 1u);
+                        }
+                      });
+}
+
+// Keys spread over the threads for the radix passes: lane l takes the
+// segment [l*seg, (l+1)*seg) of an odd length seg, wave w its offsets w,
+// w+NW, ...  A wave's 64 reads then fall in 64 different places of the key
+// array (scores are correlated with their index, so neighbouring keys share
+// digits) and in distinct LDS banks.  Needs seg <= SR * NW.
+template <int SR>
+__device__ __forceinline__ void load_spread(const uint32_t *keys, int T, uint32_t (&ks)[SR], uint32_t &valid) {
+  const int lane = threadIdx.x & 63, wv = threadIdx.x >> 6;
+  const int seg = ((T + 63) / 64) | 1;
+  valid = 0u;
+#pragma unroll
+  for (int u = 0; u < SR; ++u) {
+    const int c = wv + NW * u, i = lane * seg + c;
+    const bool ok = c < seg && i < T;
+    ks[u] = ok ? keys[i] : 0u;
+    valid |= (ok ? 1u : 0u) << u;
+  }
+}
+
+template <int SR>
+__device__ __forceinline__ uint32_t radix_threshold_regs(const uint32_t (&ks)[SR], uint32_t valid, int M,
+                                                         uint32_t kmin, uint32_t kmax, SelectShared &sh,
+                                                         int *want_out) {
+  return radix_select(M, kmin, kmax, sh, want_out,
+                      [&](unsigned *h, uint32_t pmask, uint32_t prefix, int shift, uint32_t dm) {
+#pragma unroll
+                        for (int u = 0; u < SR; ++u)
+                          if (((valid >> u) & 1u) && (ks[u] & pmask) == prefix)
+                            atomicAdd(&h[(ks[u] >> shift) & dm], 1u);
+                      });
+}
+
 // Output place of a contiguous run holding gt keys above the threshold and
 // eq equal to it, when the `want` equal keys of highest index are kept: one
 // block scan of the packed (gt, eq) pair.  *skip gets how many of the run's
@@ -155,10 +185,42 @@ __device__ __forceinline__ int kept_offset(unsigned gt, unsigned eq, int want, S
   return gt_before + max(0, eq_before - drop);
 }
 
+// Output of a contiguous run [a0, a1) whose keys are in kr: the indices of
+// those above thr, and of its share of the `want` kept ties (the highest
+// indices), ascending from the run's place in out (and out2 if non-null).
+template <int FR>
+__device__ __forceinline__ void emit_run(const uint32_t (&kr)[FR], int a0, int a1, uint32_t thr, int want,
+                                         int M, int32_t *out, int32_t *out2, SelectShared &sh) {
+  unsigned gt = 0, eq = 0;
+#pragma unroll
+  for (int u = 0; u < FR; ++u)
+    if (a0 + u < a1) {
+      gt += kr[u] > thr;
+      eq += kr[u] == thr;
+    }
+  int skip;
+  int off = kept_offset(gt, eq, want, sh, &skip);
+#pragma unroll
+  for (int u = 0; u < FR; ++u) {
+    const int i = a0 + u;
+    if (i >= a1) break;
+    bool keep = kr[u] > thr;
+    if (kr[u] == thr) {
+      if (skip > 0) --skip;
+      else keep = true;
+    }
+    if (keep && off < M) {   // off < M always holds; the guard keeps writes in bounds
+      out[off] = i;
+      if (out2 != nullptr) out2[off] = i;
+      ++off;
+    }
+  }
+}
+
 // Keep the M largest of keys[0..T) (M < T), ties to the higher index; write
 // the kept indices ascending to out (and out2 if non-null).  Thread t owns
 // the contiguous run [a0, a1) for the output.
-template <bool SEG, typename KeyPtr>
+template <typename KeyPtr>
 __device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *out, int32_t *out2,
                                            SelectShared &sh) {
   const int tid = threadIdx.x;
@@ -170,7 +232,7 @@ __device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *o
   }
   block_minmax(kmin, kmax, sh);
   int want;
-  const uint32_t thr = radix_threshold<SEG>(keys, T, M, kmin, kmax, sh, &want);
+  const uint32_t thr = radix_threshold(keys, T, M, kmin, kmax, sh, &want);
   const int per = (T + NT - 1) / NT;
   const int a0 = min(T, tid * per), a1 = min(T, a0 + per);
   unsigned gt = 0, eq = 0;
@@ -196,6 +258,32 @@ __device__ __forceinline__ void select_top(KeyPtr keys, int T, int M, int32_t *o
   }
 }
 
+// The same for T <= FR * NT keys staged in LDS, with the keys in registers:
+// the spread set for the radix passes, the contiguous run for the output.
+template <int FR>
+__device__ __forceinline__ void select_top_regs(const uint32_t *keys, int T, int M, int32_t *out,
+                                                int32_t *out2, SelectShared &sh) {
+  constexpr int SR = FR + 1;   // seg = ceil(T/64)|1 <= 16*FR + 1 <= SR * NW
+  const int tid = threadIdx.x;
+  const int per = (T + NT - 1) / NT;
+  const int a0 = min(T, tid * per), a1 = min(T, a0 + per);
+  uint32_t kr[FR], ks[SR], valid;
+  uint32_t kmin = 0xffffffffu, kmax = 0u;
+#pragma unroll
+  for (int u = 0; u < FR; ++u) {
+    kr[u] = a0 + u < a1 ? keys[a0 + u] : 0u;
+    if (a0 + u < a1) {
+      kmin = min(kmin, kr[u]);
+      kmax = max(kmax, kr[u]);
+    }
+  }
+  load_spread(keys, T, ks, valid);
+  block_minmax(kmin, kmax, sh);
+  int want;
+  const uint32_t thr = radix_threshold_regs(ks, valid, M, kmin, kmax, sh, &want);
+  emit_run<FR>(kr, a0, a1, thr, want, M, out, out2, sh);
+}
+
 __device__ __forceinline__ double class_score(int cls, double om, double a, double r) {
   if (cls == HERMES_SHALLOW) return r;
   if (cls == HERMES_DEEP) return a;
@@ -205,6 +293,8 @@ __device__ __forceinline__ double class_score(int cls, double om, double a, doub
 // Keys of layers with at most this many candidates are staged in LDS for the
 // select passes; longer layers read them from global memory (L2-resident).
 constexpr int kLdsKeys = 38400;   // 150 KiB
+// Layers of at most kRegKeys * NT candidates keep their keys in registers.
+constexpr int kRegKeys = 10;
 // Positions of the layer above with at most this many candidates are staged
 // in LDS for the partner search.
 constexpr int kLdsPos = 12288;    // 48 KiB
@@ -257,6 +347,33 @@ __device__ __forceinline__ double sum_partials(const double *p, int n) {
   return s;
 }
 
+// The same in two steps, so that the loads of up to 128 partials are issued
+// long before the sum is needed (more are summed by sum_partials itself, in
+// the same order).
+struct Partials {
+  const double *p;
+  int n;
+  double x0, x1;
+};
+
+__device__ __forceinline__ Partials load_partials(const double *p, int n) {
+  const int lane = threadIdx.x & 63;
+  Partials q;
+  q.p = p;
+  q.n = n;
+  q.x0 = (n <= 128 && lane < n) ? p[lane] : 0.0;
+  q.x1 = (n <= 128 && lane + 64 < n) ? p[lane + 64] : 0.0;
+  return q;
+}
+
+__device__ __forceinline__ double reduce_partials(Partials q) {
+  if (q.n > 128) return sum_partials(q.p, q.n);
+  double s = q.x0 + q.x1;   // the order of sum_partials: b, then b + 64
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) s += __shfl_xor(s, o);
+  return s;
+}
+
 // First index in [lo, n) of the sorted p with p[idx] >= x: a few linear
 // steps (partners of consecutive candidates are usually adjacent), then a
 // binary search.
@@ -287,107 +404,9 @@ __device__ __forceinline__ void partners(Ptr p1, int T1, const int *pv, int i0, 
       jx[u] = -1;
       continue;
     }
-    lb = lower_bound_from(p1, lb, T1, pv[u]);
+    if (u == 0 && i0 < T1 && p1[i0] == pv[0]) lb = i0;   // same physical index
+    else lb = lower_bound_from(p1, lb, T1, pv[u]);
     jx[u] = (lb < T1 && p1[lb] == pv[u]) ? lb : -1;
-  }
-}
-
-// 1. Smoothed keys of every candidate of the listed layers (Sec. 3.1 scores,
-//    Sec. 3.2 smoothing), KU consecutive candidates per thread, with the
-//    positions of the layer above staged in LDS for the partner search.
-constexpr int KT = 256;
-constexpr int KU = 4;
-__global__ __launch_bounds__(KT) void score_keys(SelectArgs a) {
-  __shared__ int32_t spos[kLdsPos];
-  const int l = a.layer_id[blockIdx.y];
-  const LayerTable &L0 = a.tab[l];
-  const int C = a.C;
-  const int T = a.len[l];
-  const int i0 = (blockIdx.x * KT + threadIdx.x) * KU;
-  if (blockIdx.x * KT * KU >= T) return;   // whole block past the layer's end
-  const int T0 = T - C;
-  const int32_t *pos = L0.pos[a.cur[l]];
-  const float *w = L0.w;
-  const int cls = L0.cls;
-  const double om = L0.omega;
-  const double lam = L0.lambda;
-  const double k = a.forget_rate;
-  const bool has_next = (l + 1 < a.n_layers) && lam != 0.0;
-  int T1 = 0, T01 = 0, cls1 = HERMES_SHALLOW;
-  const int32_t *pos1 = nullptr;
-  const float *w1 = nullptr;
-  double om1 = 0.0;
-  if (has_next) {
-    const LayerTable &L1 = a.tab[l + 1];
-    T1 = a.len[l + 1];
-    T01 = T1 - C;
-    pos1 = L1.pos[a.cur[l + 1]];
-    w1 = L1.w;
-    cls1 = L1.cls;
-    om1 = L1.omega;
-  }
-  const int am0 = a.guide_rows[l] > 0 ? 1 : a.alpha_mode;
-  const int am1 = (has_next && a.guide_rows[l + 1] > 0) ? 1 : a.alpha_mode;
-  const bool needA0 = cls != HERMES_SHALLOW, needR0 = cls != HERMES_DEEP;
-  const bool needA1 = has_next && cls1 != HERMES_SHALLOW;
-  const bool needR1 = has_next && cls1 != HERMES_DEEP;
-  const bool by_pos = has_next && a.align_mode == 0;
-  const bool pos_lds = by_pos && T1 <= kLdsPos;
-
-  int pv[KU], jx[KU];
-  float wv[KU], w1v[KU];
-#pragma unroll
-  for (int u = 0; u < KU; ++u) {
-    const int i = i0 + u;
-    const bool ok = i < T;
-    wv[u] = (ok && needA0) ? w[i] : 0.f;
-    pv[u] = (ok && by_pos) ? pos[i] : 0;
-  }
-  // every lane of the wave takes part in the butterfly: before any lane exits
-  const int nb0 = (T + kNormBlock - 1) / kNormBlock, nb1 = (T1 + kNormBlock - 1) / kNormBlock;
-  const double sa0 = needA0 ? sum_partials(a.normpart + l * a.normpart_lstride, nb0) : 0.0;
-  const double sa1 = needA1 ? sum_partials(a.normpart + (l + 1) * a.normpart_lstride, nb1) : 0.0;
-  if (pos_lds) {   // uniform over the block
-    stage_u32<KT, 12>(reinterpret_cast<const uint32_t *>(pos1), T1, reinterpret_cast<uint32_t *>(spos));
-    __syncthreads();
-  }
-  if (i0 >= T) return;
-  if (by_pos) {
-    if (pos_lds) partners<KU>(static_cast<const int32_t *>(spos), T1, pv, i0, T, jx);
-    else partners<KU>(pos1, T1, pv, i0, T, jx);
-  } else {
-#pragma unroll
-    for (int u = 0; u < KU; ++u) jx[u] = (has_next && i0 + u < T && i0 + u < T1) ? i0 + u : -1;
-  }
-#pragma unroll
-  for (int u = 0; u < KU; ++u) w1v[u] = (jx[u] >= 0 && needA1) ? w1[jx[u]] : 0.f;
-
-  const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
-  // recency normaliser in closed form: Z = (1 - e^{-kT}) / (1 - e^{-k})
-  const double z0 = expm1(-k * (double)T) / expm1(-k);
-  const double z1 = expm1(-k * (double)T1) / expm1(-k);
-  const double inv_z0 = 1.0 / z0, inv_z1 = T1 > 0 ? 1.0 / z1 : 0.0;
-  uint32_t *keys = a.keys + l * a.keys_lstride;
-#pragma unroll
-  for (int u = 0; u < KU; ++u) {
-    const int i = i0 + u;
-    if (i >= T) break;
-    const double a_i = needA0 ? mass_over_observers(wv[u], i, T0, C, am0) * inv_sa0 : 0.0;
-    const double r_i = needR0 ? exp(-k * (double)(T - 1 - i)) * inv_z0 : 0.0;
-    double st = class_score(cls, om, a_i, r_i);
-    if (has_next) {
-      double s1 = 0.0;
-      const int j = jx[u];
-      if (j >= 0) {
-        const double a_j = needA1 ? mass_over_observers(w1v[u], j, T01, C, am1) * inv_sa1 : 0.0;
-        const double r_j = needR1 ? exp(-k * (double)(T1 - 1 - j)) * inv_z1 : 0.0;
-        s1 = class_score(cls1, om1, a_j, r_j);
-      }
-      st = (1.0 - lam) * st + lam * s1;
-    }
-    const float f = (float)st;
-    keys[i] = __builtin_bit_cast(uint32_t, f);
-    if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
   }
 }
 
@@ -426,15 +445,23 @@ __device__ __forceinline__ void stage_commit(const uint32_t *src, int n, const S
   const int tid = threadIdx.x;
   const int head = stage_head(src, n);
   const int nv = (n - head) >> 2;
+  if (head == 0) {   // dst is 16-byte aligned
 #pragma unroll
-  for (int u = 0; u < R; ++u) {
-    const int q = u * NT + tid;
-    if (q < nv) {
-      uint32_t *d = dst + head + 4 * q;
-      d[0] = s.r[u].x;
-      d[1] = s.r[u].y;
-      d[2] = s.r[u].z;
-      d[3] = s.r[u].w;
+    for (int u = 0; u < R; ++u) {
+      const int q = u * NT + tid;
+      if (q < nv) reinterpret_cast<uint4 *>(dst)[q] = s.r[u];
+    }
+  } else {
+#pragma unroll
+    for (int u = 0; u < R; ++u) {
+      const int q = u * NT + tid;
+      if (q < nv) {
+        uint32_t *d = dst + head + 4 * q;
+        d[0] = s.r[u].x;
+        d[1] = s.r[u].y;
+        d[2] = s.r[u].z;
+        d[3] = s.r[u].w;
+      }
     }
   }
   if (tid < head) dst[tid] = s.h;
@@ -464,33 +491,23 @@ __device__ __forceinline__ double mass_scaled(float w, int i, int T0, int C, int
   return (double)w / (double)(C - (i - T0));
 }
 
-// Scores, smoothing and TopK of one layer in one workgroup (layers of at
-// most kFusedT candidates whose layer above has at most kFusedT): the same
-// quantities as score_keys + select_kept without the keys' round trip
-// through global memory and the second launch.
-//   1. W and positions of layers l and l+1 staged in LDS by coalesced
-//      16-byte loads, all issued before any is stored; the normalisers from
-//      the partials written with W;
-//   2. thread t scores the contiguous run of at most FR candidates it owns
-//      (the partner found from the same index or by a forward search in
-//      LDS, recency by factors of e^{k}), keys kept in registers;
-//   3. the keys go to LDS for the radix passes, then the run's kept indices
-//      go out from the registers.
-constexpr int kFusedT = 9216;
-constexpr int FR = kFusedT / NT;
+// 1. Smoothed keys S~ of every candidate of the listed layers (Sec. 3.1
+//    scores, Sec. 3.2 smoothing): workgroup (b, j) scores candidates
+//    [b*MCH, (b+1)*MCH) of layer layer_id[j], MU consecutive ones per thread
+//    (the second partner found by a forward search from the first), with
+//    the positions of the layer above staged in LDS when they fit, and
+//    writes the keys to global memory.
+constexpr int MU = 2;
+constexpr int MCH = NT * MU;
 
-__global__ __launch_bounds__(NT) void select_fused(SelectArgs a) {
-  __shared__ __align__(16) uint32_t s_w[kFusedT];     // W of layer l as bits, then the keys
-  __shared__ __align__(16) int32_t s_pos[kFusedT];    // positions of layer l
-  __shared__ __align__(16) int32_t s_pos1[kFusedT];   // positions of layer l+1
-  __shared__ __align__(16) uint32_t s_w1[kFusedT];    // W of layer l+1 as bits
-  __shared__ SelectShared sh;
+__global__ __launch_bounds__(NT) void score_keys(SelectArgs a) {
+  __shared__ __align__(16) uint32_t s_buf[kLdsPos];   // positions of layer l+1
   const int tid = threadIdx.x;
-  const int l = a.layer_id[blockIdx.x];
+  const int l = a.layer_id[blockIdx.y];
+  const int T = a.len[l];
+  if (blockIdx.x * MCH >= T) return;   // whole block past the layer's end (uniform)
   const LayerTable &L0 = a.tab[l];
   const int C = a.C;
-  const int T = a.len[l];
-  const int M = L0.budget;
   const int T0 = T - C;
   const int32_t *pos = L0.pos[a.cur[l]];
   const int cls = L0.cls;
@@ -515,108 +532,72 @@ __global__ __launch_bounds__(NT) void select_fused(SelectArgs a) {
   const bool needA1 = has_next && cls1 != HERMES_SHALLOW;
   const bool needR1 = has_next && cls1 != HERMES_DEEP;
   const bool by_pos = has_next && a.align_mode == 0;
+  const bool pos_lds = by_pos && T1 <= kLdsPos;
 
-  // 1. staging (every condition is uniform over the block)
-  {
-    Staged<3> g0, g1, g2, g3;
-    if (needA0) stage_issue(reinterpret_cast<const uint32_t *>(L0.w), T, g0);
-    if (by_pos) {
-      stage_issue(reinterpret_cast<const uint32_t *>(pos), T, g1);
-      stage_issue(reinterpret_cast<const uint32_t *>(pos1), T1, g2);
-    }
-    if (needA1) stage_issue(reinterpret_cast<const uint32_t *>(w1), T1, g3);
-    if (needA0) stage_commit(reinterpret_cast<const uint32_t *>(L0.w), T, g0, s_w);
-    if (by_pos) {
-      stage_commit(reinterpret_cast<const uint32_t *>(pos), T, g1, reinterpret_cast<uint32_t *>(s_pos));
-      stage_commit(reinterpret_cast<const uint32_t *>(pos1), T1, g2, reinterpret_cast<uint32_t *>(s_pos1));
-    }
-    if (needA1) stage_commit(reinterpret_cast<const uint32_t *>(w1), T1, g3, s_w1);
-  }
+  // loads: normaliser partials, this thread's candidates, the staged positions
   const int nb0 = (T + kNormBlock - 1) / kNormBlock, nb1 = (T1 + kNormBlock - 1) / kNormBlock;
-  const double sa0 = needA0 ? sum_partials(a.normpart + l * a.normpart_lstride, nb0) : 0.0;
-  const double sa1 = needA1 ? sum_partials(a.normpart + (l + 1) * a.normpart_lstride, nb1) : 0.0;
+  Partials q0 = {nullptr, 0, 0.0, 0.0}, q1 = {nullptr, 0, 0.0, 0.0};
+  if (needA0) q0 = load_partials(a.normpart + l * a.normpart_lstride, nb0);
+  if (needA1) q1 = load_partials(a.normpart + (l + 1) * a.normpart_lstride, nb1);
+  const int i0 = blockIdx.x * MCH + tid * MU;
+  float wv[MU];
+  int pv[MU];
+#pragma unroll
+  for (int u = 0; u < MU; ++u) {
+    const bool ok = i0 + u < T;
+    wv[u] = (ok && needA0) ? L0.w[i0 + u] : 0.f;
+    pv[u] = (ok && by_pos) ? pos[i0 + u] : 0;
+  }
+  if (pos_lds) {
+    Staged<3> g;
+    stage_issue(reinterpret_cast<const uint32_t *>(pos1), T1, g);
+    stage_commit(reinterpret_cast<const uint32_t *>(pos1), T1, g, s_buf);
+  }
+  const double sa0 = needA0 ? reduce_partials(q0) : 0.0;
+  const double sa1 = needA1 ? reduce_partials(q1) : 0.0;
   __syncthreads();
 
-  // 2. keys of this thread's run
+  // partners in layer l+1 and their W
+  int jx[MU];
+  if (pos_lds) partners<MU>(reinterpret_cast<const int32_t *>(s_buf), T1, pv, i0, T, jx);
+  else if (by_pos) partners<MU>(pos1, T1, pv, i0, T, jx);
+  else {
+#pragma unroll
+    for (int u = 0; u < MU; ++u) jx[u] = (has_next && i0 + u < T && i0 + u < T1) ? i0 + u : -1;
+  }
+  float w1v[MU];
+#pragma unroll
+  for (int u = 0; u < MU; ++u) w1v[u] = (jx[u] >= 0 && needA1) ? w1[jx[u]] : 0.f;
+
+  // keys
   const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
-  const double z0 = expm1(-k * (double)T) / expm1(-k);
-  const double z1 = expm1(-k * (double)T1) / expm1(-k);
-  const double inv_z0 = 1.0 / z0, inv_z1 = T1 > 0 ? 1.0 / z1 : 0.0;
-  const double ek = exp(k), inv_c = 1.0 / (double)C;
-  const float *s_wf = reinterpret_cast<const float *>(s_w);
-  const float *s_w1f = reinterpret_cast<const float *>(s_w1);
-  const int per = (T + NT - 1) / NT;
-  const int b0 = min(T, tid * per), e0 = min(T, b0 + per);
-  uint32_t kr[FR];
-  uint32_t kmin = 0xffffffffu, kmax = 0u;
-  int lb = 0, jp0 = -1, jp1 = -1;
+  const double inv_z0 = a.inv_z[l], inv_z1 = has_next ? a.inv_z[l + 1] : 0.0;
+  const double ek = a.ek, inv_c = a.inv_c;
+  uint32_t *keys = a.keys + l * a.keys_lstride;
+  int jp0 = -1, jp1 = -1;
   double rv0 = 0.0, rv1 = 0.0;
 #pragma unroll
-  for (int u = 0; u < FR; ++u) {
-    const int i = b0 + u;
-    kr[u] = 0u;
-    if (i >= e0) continue;
-    const double a_i = needA0 ? mass_scaled(s_wf[i], i, T0, C, am0, inv_c) * inv_sa0 : 0.0;
+  for (int u = 0; u < MU; ++u) {
+    const int i = i0 + u;
+    if (i >= T) break;
+    const double a_i = needA0 ? mass_scaled(wv[u], i, T0, C, am0, inv_c) * inv_sa0 : 0.0;
     const double r_i = needR0 ? recency_next(rv0, jp0, i, k, ek, T - 1) * inv_z0 : 0.0;
     double st = class_score(cls, om, a_i, r_i);
     if (has_next) {
-      int j = -1;
-      if (by_pos) {
-        const int p = s_pos[i];
-        if (u == 0 && i < T1 && s_pos1[i] == p) lb = i;   // same physical index
-        else lb = lower_bound_from(static_cast<const int32_t *>(s_pos1), lb, T1, p);
-        j = (lb < T1 && s_pos1[lb] == p) ? lb : -1;
-      } else {
-        j = i < T1 ? i : -1;
-      }
       double sj = 0.0;
+      const int j = jx[u];
       if (j >= 0) {
-        const double a_j = needA1 ? mass_scaled(s_w1f[j], j, T01, C, am1, inv_c) * inv_sa1 : 0.0;
+        const double a_j = needA1 ? mass_scaled(w1v[u], j, T01, C, am1, inv_c) * inv_sa1 : 0.0;
         const double r_j = needR1 ? recency_next(rv1, jp1, j, k, ek, T1 - 1) * inv_z1 : 0.0;
         sj = class_score(cls1, om1, a_j, r_j);
       }
       st = (1.0 - lam) * st + lam * sj;
     }
     const float f = (float)st;
-    kr[u] = __builtin_bit_cast(uint32_t, f);
-    kmin = min(kmin, kr[u]);
-    kmax = max(kmax, kr[u]);
+    keys[i] = __builtin_bit_cast(uint32_t, f);
     if (L0.s_dbg != nullptr) L0.s_dbg[i] = f;
   }
-  __syncthreads();   // every read of the staged W is done: s_w takes the keys
-#pragma unroll
-  for (int u = 0; u < FR; ++u)
-    if (b0 + u < e0) s_w[b0 + u] = kr[u];
-  block_minmax(kmin, kmax, sh);   // its barrier also publishes the keys
 
-  // 3. threshold, then the run's kept indices from the registers
-  int want;
-  const uint32_t thr = radix_threshold<true>(static_cast<const uint32_t *>(s_w), T, M, kmin, kmax, sh, &want);
-  unsigned gt = 0, eq = 0;
-#pragma unroll
-  for (int u = 0; u < FR; ++u)
-    if (b0 + u < e0) {
-      gt += kr[u] > thr;
-      eq += kr[u] == thr;
-    }
-  int skip;
-  int off = kept_offset(gt, eq, want, sh, &skip);
-  int32_t *kept = a.kept + l * a.kept_lstride;
-#pragma unroll
-  for (int u = 0; u < FR; ++u) {
-    const int i = b0 + u;
-    if (i >= e0) break;
-    bool keep = kr[u] > thr;
-    if (kr[u] == thr) {
-      if (skip > 0) --skip;
-      else keep = true;
-    }
-    if (keep && off < M) {   // off < M always holds; the guard keeps writes in bounds
-      kept[off] = i;
-      if (L0.kept_dbg != nullptr) L0.kept_dbg[off] = i;
-      ++off;
-    }
-  }
 }
 
 // 2. TopK of each listed layer from its keys (staged in LDS when they fit).
@@ -632,9 +613,10 @@ __global__ __launch_bounds__(NT) void select_kept(SelectArgs a) {
   if (T <= kLdsKeys) {
     stage_u32<NT, 10>(keys, T, big);
     __syncthreads();
-    select_top<true>(big, T, L0.budget, kept, L0.kept_dbg, sh);
+    if (T <= kRegKeys * NT) select_top_regs<kRegKeys>(big, T, L0.budget, kept, L0.kept_dbg, sh);
+    else select_top(static_cast<const uint32_t *>(big), T, L0.budget, kept, L0.kept_dbg, sh);
   } else {
-    select_top<false>(keys, T, L0.budget, kept, L0.kept_dbg, sh);
+    select_top(keys, T, L0.budget, kept, L0.kept_dbg, sh);
   }
 }
 
@@ -644,24 +626,15 @@ __global__ __launch_bounds__(NT) void topk_keys(const uint32_t *keys, int n, int
     for (int i = threadIdx.x; i < n; i += NT) out[i] = i;
     return;
   }
-  select_top<false>(keys, n, k, out, nullptr, sh);
+  select_top(keys, n, k, out, nullptr, sh);
 }
 
 }  // namespace
 
 hipError_t launch_select(const SelectArgs &a, hipStream_t s) {
-  bool fused = true;
-  for (int j = 0; j < a.n_list; ++j) {
-    const int l = a.layer_id[j];
-    fused = fused && a.len[l] <= kFusedT && (l + 1 >= a.n_layers || a.len[l + 1] <= kFusedT);
-  }
-  if (fused) {
-    hipLaunchKernelGGL(select_fused, dim3(a.n_list), dim3(NT), 0, s, a);
-    return hipGetLastError();
-  }
   int max_T = 0;
   for (int j = 0; j < a.n_list; ++j) max_T = max(max_T, a.len[a.layer_id[j]]);
-  hipLaunchKernelGGL(score_keys, dim3((max_T + KT * KU - 1) / (KT * KU), a.n_list), dim3(KT), 0, s, a);
+  hipLaunchKernelGGL(score_keys, dim3((max_T + MCH - 1) / MCH, a.n_list), dim3(NT), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(select_kept, dim3(a.n_list), dim3(NT), 0, s, a);
