@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # and WRITE_SIZE counter passes in profiles/traffic_c3_7b_28layer.md (fetch
 # scaled x2.000, write x1.000 by a 256 MiB copy).  Valid only for the kernel
 # source it was measured on: reported as null once attention.hip changes.
-ATTN_TRAFFIC = {"bytes": 1.4225e9, "source_sha256_16": "6579f46e6310ab88",
+ATTN_TRAFFIC = {"bytes": 1.4204e9, "source_sha256_16": "4579fe6440dad7cb",
                 "workload": "c3_7b_28layer"}
 
 
@@ -58,6 +58,19 @@ def gather_bytes(wl) -> float:
     T = wl.init_len + wl.chunk
     kept = sum(min(T, b) for b in wl.budgets if T > b)
     return kept * (4.0 * row + 8.0)
+
+
+def select_bytes(wl) -> float:
+    """Algorithmic bytes of scoring + top-k: W and positions of every
+    evicting layer and of the layer above it read once, the kept list
+    written (the fp32 keys round trip between the two select launches is
+    working memory, not counted)."""
+    T = wl.init_len + wl.chunk
+    n = 0.0
+    for l, b in enumerate(wl.budgets):
+        if T > b:
+            n += 8.0 * T + (8.0 * T if l + 1 < wl.n_layers else 0.0) + 4.0 * b
+    return n
 
 
 def attn_traffic(wl):
@@ -179,6 +192,11 @@ def main() -> int:
         g = gb / (kernels["gather"]["avg_ms"] * 1e-3) / 1e9
         extra["gather_GBps"] = round(g, 1)
         extra["gather_hbm_frac"] = round(g / PEAK_HBM_GBS, 4)
+    if "gather" in kernels and "select" in kernels:
+        sc_ms = kernels["select"]["avg_ms"] + kernels["gather"]["avg_ms"]
+        sc = (gb + select_bytes(wl)) / (sc_ms * 1e-3) / 1e9
+        extra["select_compaction"] = {"ms": round(sc_ms, 4), "bytes": gb + select_bytes(wl),
+                                      "GBps": round(sc, 1), "hbm_frac": round(sc / PEAK_HBM_GBS, 4)}
     if "colsum" in kernels:
         sweep = attention_flops(wl) / 2 * _mass_layer_fraction(wl)
         extra["colsum_TFLOPs_executed"] = round(sweep / (kernels["colsum"]["avg_ms"] * 1e-3) / 1e12, 2)
