@@ -383,7 +383,7 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
 }
 
 template <int D>
-__global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
+__global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   const int kblk = lin % nkb;
   const int kv_blk = (lin / nkb) % a.Hkv;
@@ -422,8 +422,8 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
   const float *lse_l = a.lse + layer * a.lse_lstride;
   const float c = a.scale_log2;
 
-  // Three-deep ring of 32-row query tiles: tile it+1 is read by the MFMAs
-  // while tile it's probabilities are summed and tile it+2 is stored.
+  // Three-deep ring of 32-row query tiles: tile it is read by the MFMAs
+  // while tile it+2 is stored and tile it+3 loaded.
   __shared__ __attribute__((aligned(16))) uint16_t Qs[3][BQS][D + KPAD];
   __shared__ __attribute__((aligned(16))) float Ls[3][BQS];
 
@@ -431,22 +431,34 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
   constexpr int NLD = BQS * CH / 256;
   uint4 qreg[NLD];
   float lreg = INFINITY;
-  auto tile_kv = [&](int) { return kv_blk; };
   auto tile_p = [&](int it) { return p_begin + it * BQS; };
+  // Tiles are loaded in order, so each thread's packed rows p = (r, g) step
+  // by BQS per tile without a division by G.
+  int ld_p[NLD], ld_r[NLD], ld_g[NLD];
+  const int step_r = BQS / G, step_g = BQS - (BQS / G) * G;
+#pragma unroll
+  for (int u = 0; u < NLD; ++u) {
+    ld_p[u] = p_begin + (tid + u * 256) / CH;
+    ld_r[u] = ld_p[u] / G;
+    ld_g[u] = ld_p[u] - ld_r[u] * G;
+  }
   auto load_tile = [&](int it) {
-    const int kv = tile_kv(it), pt = tile_p(it);
+    const int pt = tile_p(it);
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
       const int e = tid + u * 256;
-      const int p = pt + e / CH;
       uint4 v = {0u, 0u, 0u, 0u};
-      if (p < P) {
-        const int r = p / G, g = p - (p / G) * G;
-        v = gload16(q + ((int64_t)r * Hq + kv * G + g) * D + (e % CH) * 8);
-      }
+      if (ld_p[u] < P) v = gload16(q + ((int64_t)ld_r[u] * Hq + kv_blk * G + ld_g[u]) * D + (e % CH) * 8);
       qreg[u] = v;
+      ld_p[u] += BQS;
+      ld_r[u] += step_r;
+      ld_g[u] += step_g;
+      if (ld_g[u] >= G) {
+        ld_g[u] -= G;
+        ++ld_r[u];
+      }
     }
-    if (tid < BQS) lreg = (pt + tid < P) ? lse_l[(int64_t)kv * P + pt + tid] : INFINITY;
+    if (tid < BQS) lreg = (pt + tid < P) ? lse_l[(int64_t)kv_blk * P + pt + tid] : INFINITY;
   };
   auto store_tile = [&](int it) {
     const int b = it % 3;
@@ -529,11 +541,13 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
   }
   if (nit > 2) load_tile(2);
   __syncthreads();
-  f32x16 s_cur[2], s_nxt[2];
-  scores(0, s_cur);
+  // One tile per trip, scores then probabilities: without a second score
+  // buffer the kernel fits three waves per SIMD, which hide the MFMA and LDS
+  // latency better than overlapping two tiles inside one wave did.
+  f32x16 s_cur[2];
   auto step = [&](int it, auto masked) {
     float lv[16];
-    if (it + 1 < nit) scores(it + 1, s_nxt);
+    scores(it, s_cur);
     read_lse(it, lv);
     if constexpr (decltype(masked)::value) acc_masked(it, s_cur, lv); else acc_plain(s_cur, lv);
     if (it + 2 < nit) {
@@ -541,22 +555,18 @@ __global__ __launch_bounds__(256, 2) void attn_colsum(ColsumArgs a, int nkb) {
       if (it + 3 < nit) load_tile(it + 3);
     }
     __syncthreads();
-    s_cur[0] = s_nxt[0];
-    s_cur[1] = s_nxt[1];
   };
   int it = 0;
   for (; it < n_mask; ++it) step(it, std::integral_constant<bool, true>{});
   // steady state: no branches inside the body
   for (; it + 3 < nit; ++it) {
     float lv[16];
-    scores(it + 1, s_nxt);
+    scores(it, s_cur);
     read_lse(it, lv);
     acc_plain(s_cur, lv);
     store_tile(it + 2);
     load_tile(it + 3);
     __syncthreads();
-    s_cur[0] = s_nxt[0];
-    s_cur[1] = s_nxt[1];
   }
   for (; it < nit; ++it) step(it, std::integral_constant<bool, false>{});
   double *part = a.wpart + layer * a.wpart_lstride + (int64_t)kv_blk * a.wpart_hstride;

@@ -495,13 +495,14 @@ __device__ __forceinline__ double mass_scaled(float w, int i, int T0, int C, int
 //    scores, Sec. 3.2 smoothing): workgroup (b, j) scores candidates
 //    [b*MCH, (b+1)*MCH) of layer layer_id[j], MU consecutive ones per thread
 //    (the second partner found by a forward search from the first), with
-//    the positions of the layer above staged in LDS when they fit, and
-//    writes the keys to global memory.
+//    the positions and W of the layer above staged in LDS when they fit,
+//    and writes the keys to global memory.
 constexpr int MU = 2;
 constexpr int MCH = NT * MU;
 
 __global__ __launch_bounds__(NT) void score_keys(SelectArgs a) {
   __shared__ __align__(16) uint32_t s_buf[kLdsPos];   // positions of layer l+1
+  __shared__ __align__(16) uint32_t s_w1[kLdsPos];    // W of layer l+1 as bits
   const int tid = threadIdx.x;
   const int l = a.layer_id[blockIdx.y];
   const int T = a.len[l];
@@ -548,10 +549,13 @@ __global__ __launch_bounds__(NT) void score_keys(SelectArgs a) {
     wv[u] = (ok && needA0) ? L0.w[i0 + u] : 0.f;
     pv[u] = (ok && by_pos) ? pos[i0 + u] : 0;
   }
-  if (pos_lds) {
-    Staged<3> g;
-    stage_issue(reinterpret_cast<const uint32_t *>(pos1), T1, g);
-    stage_commit(reinterpret_cast<const uint32_t *>(pos1), T1, g, s_buf);
+  const bool w1_lds = needA1 && T1 <= kLdsPos;
+  {
+    Staged<3> g, h;
+    if (pos_lds) stage_issue(reinterpret_cast<const uint32_t *>(pos1), T1, g);
+    if (w1_lds) stage_issue(reinterpret_cast<const uint32_t *>(w1), T1, h);
+    if (pos_lds) stage_commit(reinterpret_cast<const uint32_t *>(pos1), T1, g, s_buf);
+    if (w1_lds) stage_commit(reinterpret_cast<const uint32_t *>(w1), T1, h, s_w1);
   }
   const double sa0 = needA0 ? reduce_partials(q0) : 0.0;
   const double sa1 = needA1 ? reduce_partials(q1) : 0.0;
@@ -567,7 +571,10 @@ __global__ __launch_bounds__(NT) void score_keys(SelectArgs a) {
   }
   float w1v[MU];
 #pragma unroll
-  for (int u = 0; u < MU; ++u) w1v[u] = (jx[u] >= 0 && needA1) ? w1[jx[u]] : 0.f;
+  for (int u = 0; u < MU; ++u)
+    w1v[u] = (jx[u] >= 0 && needA1)
+                 ? (w1_lds ? __builtin_bit_cast(float, s_w1[jx[u]]) : w1[jx[u]])
+                 : 0.f;
 
   // keys
   const double inv_sa0 = sa0 > 0.0 ? 1.0 / sa0 : 0.0, inv_sa1 = sa1 > 0.0 ? 1.0 / sa1 : 0.0;
@@ -613,7 +620,22 @@ __global__ __launch_bounds__(NT) void select_kept(SelectArgs a) {
   if (T <= kLdsKeys) {
     stage_u32<NT, 10>(keys, T, big);
     __syncthreads();
-    if (T <= kRegKeys * NT) select_top_regs<kRegKeys>(big, T, L0.budget, kept, L0.kept_dbg, sh);
+    if (T <= kRegKeys * NT) {
+      // keys in registers: big is free once the radix passes are done and
+      // takes the kept list, written out coalesced
+      select_top_regs<kRegKeys>(big, T, L0.budget, reinterpret_cast<int32_t *>(big), nullptr, sh);
+      __syncthreads();
+      const int M = L0.budget;   // < T <= kRegKeys * NT
+#pragma unroll
+      for (int u = 0; u < kRegKeys; ++u) {
+        const int i = u * NT + threadIdx.x;
+        if (i < M) {
+          const int32_t x = static_cast<int32_t>(big[i]);
+          kept[i] = x;
+          if (L0.kept_dbg != nullptr) L0.kept_dbg[i] = x;
+        }
+      }
+    }
     else select_top(static_cast<const uint32_t *>(big), T, L0.budget, kept, L0.kept_dbg, sh);
   } else {
     select_top(keys, T, L0.budget, kept, L0.kept_dbg, sh);
