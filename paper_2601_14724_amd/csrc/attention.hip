@@ -32,6 +32,8 @@ constexpr int BK = kColsumKeysPerBlock;  // candidates per sweep workgroup (4 wa
 constexpr int BQS = 32;                  // packed rows per sweep tile
 constexpr int KPAD = 8;                  // u16 padding of K / Q rows in LDS
 constexpr int VPAD = 32;                 // u16 padding of V rows in LDS
+constexpr int kAheadK = 4;               // K fragment reads issued ahead of their MFMA
+constexpr int kAheadV = 4;               // V^T fragment pairs issued ahead of their MFMA
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -202,6 +204,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
         s[sub] = mfma32(kf, qf[kk], s[sub]);
       }
     }
+    // Schedule: kAheadK fragment reads, then one MFMA per read, so each MFMA's
+    // operand was requested kAheadK MFMAs earlier (3% faster on the 7B
+    // workload than all reads first).
+#pragma unroll
+    for (int i = 0; i < kAheadK; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+    for (int i = 0; i < 2 * (D / 16) - kAheadK; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < kAheadK; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
     if constexpr (decltype(masked)::value) {
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
@@ -258,6 +272,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
         o[db] = mfma32(vf, pf[qq], o[db]);
       }
     }
+    // the same for O^T += V^T P^T: two transposed reads per MFMA, kAheadV
+    // MFMAs ahead
+    constexpr int kPV = (D / 32) * 4;
+#pragma unroll
+    for (int i = 0; i < 2 * kAheadV; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 1);
+#pragma unroll
+    for (int i = 0; i < kPV - kAheadV; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
+      __builtin_amdgcn_sched_group_barrier(0x100, 2, 1);
+    }
+#pragma unroll
+    for (int i = 0; i < kAheadV; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 1);
   };
 
   using NoMask = std::integral_constant<bool, false>;
