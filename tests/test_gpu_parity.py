@@ -129,3 +129,19 @@ def test_determinism_bitwise():
         kv.close()
     for a, b in zip(*res):
         assert np.array_equal(a, b)
+
+
+def test_degenerate_budgets_keep_one_evict_one_keep_all():
+    """Budgets 1 (keep one candidate), T - 1 (evict exactly one) and T (keep
+    everything) on the same step."""
+    wl = wk.custom("degenerate", 122, 3, 4, 2, 64, 200, 40, [1, 239, 240])
+    _step_parity(wl, classes=[orc.MIDDLE, orc.DEEP, orc.DEEP])
+
+
+def test_long_layers_past_the_lds_staging_limits():
+    """40000 cached + 32 new candidates: the selection keys no longer fit in
+    LDS (read from global memory), the partner positions of the layer above
+    are searched in global memory, and the normaliser has more partials than
+    one wave loads at once."""
+    wl = wk.custom("long", 123, 2, 2, 1, 64, 40000, 32, [20000, 30000])
+    _step_parity(wl, classes=[orc.MIDDLE, orc.DEEP])
