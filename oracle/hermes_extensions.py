@@ -21,7 +21,12 @@ What it computes (arXiv 2601.14724):
     appendix "Guidance Prompt"): the attention mass W comes from the prompt's
     query rows placed after every cached token, instead of from the chunk;
   * layer-weighted budget allocation (Sec. 4 ablation "Layer-dependent Memory
-    Budget"): m_i = floor(w_i / sum_j w_j * |M|), residue to the last layer.
+    Budget"): m_i = floor(w_i / sum_j w_j * |M|), residue to the last layer;
+  * 3D M-RoPE re-indexing (appendix "Re-indexing for Qwen2.5-VL (3D
+    M-RoPE)", its three equations): every axis d in {t, h, w} is left-
+    compacted on its own, p_new^(d) = offset + rank of p_old^(d) among the
+    layer's retained coordinates on that axis, and every cached key is
+    rotated section by section by e^{i (p_new^(d) - p_old^(d)) theta^(d)}.
 
 Readings where the paper is silent (each listed in the design notes):
   * RoPE uses the rotate-half channel layout (pairs (j, j + d/2)) with
@@ -40,6 +45,13 @@ Readings where the paper is silent (each listed in the design notes):
     physical order, p_new = offset + j; eager mode re-indexes every layer at
     every compression, lazy mode re-indexes every layer when the largest
     retained position of any layer plus a headroom reaches the limit;
+  * 3D M-RoPE: the d/2 frequency pairs (frequencies theta^(-2j/d) as in
+    1D) are split into three contiguous sections, t first, then h, then w,
+    with the section sizes an input (by default a quarter of the pairs for t
+    and the rest halved between h and w: 16/24/24 at d = 128, the backbone's
+    split); the rank on an axis counts DISTINCT retained coordinates, so
+    tokens that shared a coordinate still share it; the same offset applies
+    to every axis; summary tokens are not combined with 3D coordinates;
   * guidance rows attend every token of the cache and their own earlier rows
     (the prompt follows the video); only the cached tokens are candidates and
     every one of them is seen by all prompt rows, so alpha_mode 0 divides by
@@ -130,6 +142,59 @@ def reindex_keys(k: np.ndarray, rpos: np.ndarray, offset: int,
 
 
 # --------------------------------------------------------------------------
+# 3D M-RoPE re-indexing (appendix, Qwen2.5-VL: its three equations)
+# --------------------------------------------------------------------------
+
+def default_mrope_section(head_dim: int):
+    """Frequency pairs per axis (t, h, w): a quarter of the d/2 pairs for t,
+    the rest halved between h and w (16/24/24 at d = 128)."""
+    half = head_dim // 2
+    t = half // 4
+    h = (half - t) // 2
+    return (t, h, half - t - h)
+
+
+def mrope_pair_axis(head_dim: int, section) -> np.ndarray:
+    """Axis (0 = t, 1 = h, 2 = w) of each of the d/2 frequency pairs."""
+    s = [int(x) for x in section]
+    assert len(s) == 3 and min(s) >= 0 and sum(s) == head_dim // 2, section
+    return np.repeat(np.arange(3), s)
+
+
+def rotary_delta3(k: np.ndarray, delta3: np.ndarray, section,
+                  theta: float = DEFAULT_ROPE_THETA) -> np.ndarray:
+    """k [n][H][d] times the concatenation over the sections of
+    e^{i delta^(d) theta^(d)}: pair j turns by delta[axis(j)] * theta_j."""
+    d = k.shape[-1]
+    half = d // 2
+    axis = mrope_pair_axis(d, section)
+    ang = np.asarray(delta3, dtype=np.float64)[:, axis] * inv_freq(d, theta)[None, :]
+    c = np.cos(ang)[:, None, :]
+    s = np.sin(ang)[:, None, :]
+    re, im = k[..., :half], k[..., half:]
+    return np.concatenate([re * c - im * s, im * c + re * s], axis=-1)
+
+
+def reindex_coords3(coords: np.ndarray, offset: int) -> np.ndarray:
+    """p_new^(d) = offset + rank of p_old^(d) in the sorted set of the
+    retained coordinates on axis d, for d = t, h, w independently."""
+    coords = np.asarray(coords, dtype=np.int64)
+    out = np.empty_like(coords)
+    for a in range(3):
+        values = np.unique(coords[:, a])          # the sorted set P^(d)
+        out[:, a] = offset + np.searchsorted(values, coords[:, a])
+    return out
+
+
+def reindex_keys3(k: np.ndarray, coords: np.ndarray, offset: int, section,
+                  theta: float = DEFAULT_ROPE_THETA):
+    """k_new = k_old * RotaryDelta(p_old, p_new) section by section, stored
+    as bfloat16; returns (keys, new coordinates)."""
+    new = reindex_coords3(coords, offset)
+    return round_to_bf16(rotary_delta3(k, new - np.asarray(coords, dtype=np.int64), section, theta)), new
+
+
+# --------------------------------------------------------------------------
 # guidance-prompt pseudo-query (Sec. 3.1 deep layers, appendix prompts)
 # --------------------------------------------------------------------------
 
@@ -187,6 +252,8 @@ class ExtConfig:
     rope_limit: int = 1 << 30          # lazy mode: the model's position limit
     rope_headroom: int = 0             # lazy mode: positions kept free below it
     scoring_mode: int = SCORE_CHUNK    # W from the chunk or from a guidance prompt
+    rope_axes: int = 1                 # 1: one RoPE position; 3: M-RoPE (t, h, w)
+    mrope_section: tuple = ()          # pairs per axis; () = default_mrope_section(d)
 
 
 @dataclasses.dataclass
@@ -195,6 +262,8 @@ class ExtLayerCache:
     v: np.ndarray
     pos: np.ndarray    # [T] stream positions (token identity), strictly increasing
     rpos: np.ndarray   # [T] RoPE positions the stored keys carry, strictly increasing
+                       # (3D: the t coordinates, non-decreasing)
+    rpos3: Optional[np.ndarray] = None   # [T][3] (t, h, w) coordinates in 3D mode
 
 
 def stream_step_ext(caches: List[ExtLayerCache], chunks: List[dict], cfg: ho.OracleConfig,
@@ -218,10 +287,17 @@ def stream_step_ext(caches: List[ExtLayerCache], chunks: List[dict], cfg: ho.Ora
         else:
             o, w = None, None
         outs.append(o)
-        rp = np.asarray(ch.get("rope_pos", ch["pos"]), dtype=np.int64)
-        cats.append(ExtLayerCache(np.concatenate([c.k, ch["k"]]), np.concatenate([c.v, ch["v"]]),
-                                  np.concatenate([c.pos, ch["pos"]]).astype(np.int64),
-                                  np.concatenate([c.rpos, rp]).astype(np.int64)))
+        if ext.rope_axes == 3:
+            thw = np.asarray(ch["rope_thw"], dtype=np.int64).T          # [C][3]
+            r3 = np.concatenate([c.rpos3, thw]).astype(np.int64)
+            cats.append(ExtLayerCache(np.concatenate([c.k, ch["k"]]), np.concatenate([c.v, ch["v"]]),
+                                      np.concatenate([c.pos, ch["pos"]]).astype(np.int64),
+                                      r3[:, 0].copy(), r3))
+        else:
+            rp = np.asarray(ch.get("rope_pos", ch["pos"]), dtype=np.int64)
+            cats.append(ExtLayerCache(np.concatenate([c.k, ch["k"]]), np.concatenate([c.v, ch["v"]]),
+                                      np.concatenate([c.pos, ch["pos"]]).astype(np.int64),
+                                      np.concatenate([c.rpos, rp]).astype(np.int64)))
         if ext.scoring_mode == SCORE_GUIDANCE and cfg.classes[l] != ho.SHALLOW and compute_attention:
             p = prompts[l]
             w = guidance_mass(p["q"], cats[l].k, cats[l].v, p["k"], p["v"], cfg.sm_scale)
@@ -262,6 +338,9 @@ def compact_layer(cat: ExtLayerCache, idx: np.ndarray, deep: bool, ext: ExtConfi
     evicted rows at the sorted place of the newest evicted token."""
     T = cat.k.shape[0]
     k, v, pos, rpos = cat.k[idx], cat.v[idx], cat.pos[idx], cat.rpos[idx]
+    if ext.rope_axes == 3:
+        assert not ext.summary, "summary tokens are not combined with 3D coordinates"
+        return ExtLayerCache(k, v, pos, rpos, cat.rpos3[idx]), None
     summ = None
     if ext.summary and deep and len(idx) < T:
         mask = np.ones(T, dtype=bool)
@@ -286,11 +365,20 @@ def reindex_layers(compact: List[ExtLayerCache], ext: ExtConfig):
     if ext.reindex_mode == REINDEX_EAGER:
         reindexed = True
     elif ext.reindex_mode == REINDEX_LAZY:
-        top = max(int(c.rpos[-1]) for c in compact if len(c.rpos))
+        if ext.rope_axes == 3:
+            top = max(int(c.rpos3.max()) for c in compact if len(c.rpos))
+        else:
+            top = max(int(c.rpos[-1]) for c in compact if len(c.rpos))
         reindexed = top + ext.rope_headroom >= ext.rope_limit
     if not reindexed:
         return compact, False
     out = []
+    if ext.rope_axes == 3:
+        for c in compact:
+            section = ext.mrope_section or default_mrope_section(c.k.shape[-1])
+            k_new, r_new = reindex_keys3(c.k, c.rpos3, ext.rope_offset, section, ext.rope_theta)
+            out.append(ExtLayerCache(k_new, c.v, c.pos, r_new[:, 0].copy(), r_new))
+        return out, True
     for c in compact:
         k_new, r_new = reindex_keys(c.k, c.rpos, ext.rope_offset, ext.rope_theta)
         out.append(ExtLayerCache(k_new, c.v, c.pos, r_new))

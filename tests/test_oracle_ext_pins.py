@@ -237,3 +237,122 @@ def test_ext_step_guidance_zero_queries_keep_newest_in_deep_layers():
     for l in (2, 3):
         assert np.allclose(res["w"][l], res["w"][l][0], rtol=1e-14)
         assert list(res["kept"][l]) == list(range(22, 52))
+
+
+# ---------------------------------------------------------------- 3D M-RoPE
+
+def _grid(frames, H, W, offset=0, t_step=1):
+    """(t, h, w) of a video laid out frame by frame, row by row (the order
+    tokens are appended in), written out here independently of the oracle."""
+    out = []
+    for f in range(frames):
+        for y in range(H):
+            for x in range(W):
+                out.append((offset + f * t_step, offset + y, offset + x))
+    return np.array(out, dtype=np.int64)
+
+
+def test_mrope_with_one_section_reduces_to_1d():
+    """All pairs in the t section: the sectioned rotation is the 1D rotation
+    by the t delta, and ranking strictly increasing t is the 1D rank."""
+    k = _raw(9, 2, 16)
+    d3 = np.stack([RNG.integers(-50, 50, 9), RNG.integers(-50, 50, 9), RNG.integers(-50, 50, 9)], 1)
+    assert np.array_equal(he.rotary_delta3(k, d3, (8, 0, 0)), he.rotary_delta(k, d3[:, 0]))
+    t = np.sort(RNG.choice(1000, 9, replace=False))
+    c = np.stack([t, RNG.integers(0, 5, 9), RNG.integers(0, 5, 9)], 1)
+    assert np.array_equal(he.reindex_coords3(c, 7)[:, 0], he.reindex_positions(t, 7))
+
+
+def test_mrope_full_grid_is_unchanged():
+    g = _grid(3, 4, 5, offset=11)
+    assert np.array_equal(he.reindex_coords3(g, 11), g)
+    k = he.round_to_bf16(_raw(len(g), 2, 32))
+    kn, new = he.reindex_keys3(k, g, 11, (4, 6, 6))
+    assert np.array_equal(kn, k) and np.array_equal(new, g)
+
+
+def test_mrope_dropping_a_frame_and_a_column():
+    """Frame 1 and column 2 evicted everywhere: later frames move one step
+    down in t, later columns one step down in w, rows keep their h."""
+    F, H, W, off = 4, 3, 5, 2
+    g = _grid(F, H, W, offset=off)
+    f = (g[:, 0] - off)
+    x = (g[:, 2] - off)
+    keep = (f != 1) & (x != 2)
+    new = he.reindex_coords3(g[keep], off)
+    exp_t = off + np.where(f[keep] > 1, f[keep] - 1, f[keep])
+    exp_w = off + np.where(x[keep] > 2, x[keep] - 1, x[keep])
+    assert np.array_equal(new[:, 0], exp_t)
+    assert np.array_equal(new[:, 1], g[keep][:, 1])
+    assert np.array_equal(new[:, 2], exp_w)
+
+
+def test_mrope_ranks_are_dense_and_shared_coordinates_stay_shared():
+    c = np.stack([RNG.integers(0, 40, 200) * 3, RNG.integers(0, 9, 200) + 100, RNG.integers(5, 30, 200)], 1)
+    new = he.reindex_coords3(c, 4)
+    for a in range(3):
+        distinct = sorted(set(c[:, a].tolist()))
+        assert sorted(set(new[:, a].tolist())) == list(range(4, 4 + len(distinct)))
+        for i in range(0, 200, 7):
+            for j in range(0, 200, 11):
+                assert (c[i, a] < c[j, a]) == (new[i, a] < new[j, a])
+                assert (c[i, a] == c[j, a]) == (new[i, a] == new[j, a])
+
+
+def test_mrope_reindexed_keys_equal_keys_made_at_new_coordinates():
+    """A raw key made at 3D coordinates p by multiplying each complex pair
+    (x_j + i x_{j+d/2}) by e^{i p_axis(j) theta_j}, computed here with complex
+    exponentials; the oracle's RotaryDelta from old to new coordinates turns
+    the key made at the old coordinates into the one made at the new."""
+    d, section = 32, (4, 6, 6)
+    axis = np.array([0] * section[0] + [1] * section[1] + [2] * section[2])
+    freq = 1.0e6 ** (-np.arange(d // 2) * 2.0 / d)
+
+    def made_at(x, p):
+        z = x[..., : d // 2] + 1j * x[..., d // 2:]
+        z = z * np.exp(1j * p[:, axis][:, None, :] * freq[None, None, :])
+        return np.concatenate([z.real, z.imag], axis=-1)
+
+    g = _grid(3, 4, 4, offset=9)
+    keep = RNG.random(len(g)) < 0.6
+    old = g[keep]
+    x = _raw(len(old), 2, d)
+    new = he.reindex_coords3(old, 9)
+    moved = he.rotary_delta3(made_at(x, old), new - old, section)
+    assert np.abs(moved - made_at(x, new)).max() < 1e-12
+
+
+def _tiny_mrope(L=3, frames0=4, frames=1, H=3, W=4, Hq=4, Hkv=2, d=16, budgets=(30, 30, 30), seed=5):
+    rng = np.random.default_rng(seed)
+    r = lambda *s: he.round_to_bf16(rng.standard_normal(s) * 0.5)
+    T0, C = frames0 * H * W, frames * H * W
+    g = _grid(frames0 + frames, H, W, offset=3)
+    caches = [he.ExtLayerCache(r(T0, Hkv, d), r(T0, Hkv, d), np.arange(T0), g[:T0, 0].copy(), g[:T0].copy())
+              for _ in range(L)]
+    chunks = [{"q": r(C, Hq, d), "k": r(C, Hkv, d), "v": r(C, Hkv, d), "pos": np.arange(T0, T0 + C),
+               "rope_thw": g[T0:].T.copy()} for _ in range(L)]
+    cfg = ho.OracleConfig(budgets=list(budgets), classes=[ho.SHALLOW, ho.MIDDLE, ho.DEEP])
+    return caches, chunks, cfg, g
+
+
+def test_ext_step_mrope_eager_and_lazy():
+    caches, chunks, cfg, g = _tiny_mrope()
+    ext = he.ExtConfig(reindex_mode=he.REINDEX_EAGER, rope_offset=3, rope_axes=3)
+    res = he.stream_step_ext(caches, chunks, cfg, ext)
+    assert res["reindexed"]
+    plain = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(rope_axes=3))
+    for l in range(3):
+        c, p = res["caches"][l], plain["caches"][l]
+        assert np.array_equal(c.pos, p.pos) and np.array_equal(c.v, p.v)
+        assert np.array_equal(p.rpos3, g[res["kept"][l]])
+        for a in range(3):
+            n = len(set(p.rpos3[:, a].tolist()))
+            assert sorted(set(c.rpos3[:, a].tolist())) == list(range(3, 3 + n))
+    # largest retained coordinate is t = 3 + 4 = 7: the lazy rule fires at 7 + 2 >= limit
+    no = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(reindex_mode=he.REINDEX_LAZY, rope_axes=3,
+                                                              rope_limit=10, rope_headroom=2))
+    yes = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(reindex_mode=he.REINDEX_LAZY, rope_axes=3,
+                                                               rope_limit=9, rope_headroom=2, rope_offset=3))
+    assert not no["reindexed"] and yes["reindexed"]
+    for l in range(3):
+        assert np.array_equal(yes["caches"][l].k, res["caches"][l].k)
