@@ -111,10 +111,24 @@ typedef struct {
                               RoPE position of any layer + headroom >= limit      */
   double rope_theta;       /* RoPE base; <= 0 selects 1e6                          */
   int32_t scoring_mode;    /* HERMES_SCORE_*: source of the attention mass W      */
+  int32_t rope_axes;       /* 1 (0 reads as 1): one RoPE position per token (rpos);
+                              3: M-RoPE (t, h, w) coordinates, t in rpos and h, w
+                              in rpos_h / rpos_w, chunks appended through
+                              hermes_append_chunk_mrope (appendix, 3D M-RoPE
+                              re-indexing); needs summary_mode 0                 */
+  int32_t mrope_section[3];/* rope_axes 3: frequency pairs j = 0 .. head_dim/2 - 1
+                              of the t, h and w sections, in that order (sum
+                              head_dim/2); all 0 selects head_dim/8 pairs for t
+                              and the rest halved between h and w (16, 24, 24 at
+                              head_dim 128)                                        */
 } hermes_config;
 
 /* Position re-indexing (Sec. 3.3; appendix, 1D RoPE re-indexing). */
 enum { HERMES_REINDEX_NONE = 0, HERMES_REINDEX_EAGER = 1, HERMES_REINDEX_LAZY = 2 };
+/* 3D re-indexing ranks the coordinates of one layer on one axis when they
+ * span at most this many values (max - min + 1); a wider axis keeps its
+ * coordinates, and the key sections it drives are not turned. */
+enum { HERMES_MROPE_MAX_SPAN = 262144 };
 /* Source of W: the chunk's own queries (default) or a guidance prompt used as
  * a pseudo-query (Sec. 3.1 deep-layer paragraph; appendix guidance prompts). */
 enum { HERMES_SCORE_CHUNK = 0, HERMES_SCORE_GUIDANCE = 1 };
@@ -136,7 +150,11 @@ enum { HERMES_SCORE_CHUNK = 0, HERMES_SCORE_GUIDANCE = 1 };
  *  rpos[2]      int32 [cap] RoPE positions the stored keys were rotated with,
  *               one per buffer, strictly increasing along the cache; buffer 0
  *               holds the initial `init_len` values.  Required (non-NULL) when
- *               summary_mode or reindex_mode is on, else ignored (may be NULL).
+ *               summary_mode or reindex_mode is on, or rope_axes is 3, else
+ *               ignored (may be NULL).  With rope_axes 3: the t coordinates.
+ *  rpos_h[2], rpos_w[2]
+ *               rope_axes 3: int32 [cap] h and w coordinates, laid out like
+ *               rpos (buffer 0 holds the initial values); else ignored.
  */
 typedef struct {
   void *k[2];
@@ -148,6 +166,8 @@ typedef struct {
   int32_t cap;
   int32_t init_len;
   int32_t *rpos[2];
+  int32_t *rpos_h[2];
+  int32_t *rpos_w[2];
 } hermes_layer_buffers;
 
 /* Bytes of device workspace hermes_kv_init needs for `cfg` (0 on a bad cfg). */
@@ -193,6 +213,19 @@ int hermes_append_chunk_at(hermes_ctx *ctx, int32_t layer, const void *q, const 
                            int32_t n_new, void *out, void *stream);
 
 /*
+ * hermes_append_chunk for M-RoPE coordinates (rope_axes 3; appendix, 3D
+ * M-RoPE re-indexing): rope_thw is device int32 [3][n_new], the t, then the
+ * h, then the w coordinate of every new row (the same for every layer with
+ * HERMES_ALL_LAYERS), stored in rpos / rpos_h / rpos_w; the chunk's keys
+ * carry these coordinates.  The plain appends are refused (ESTATE) when
+ * rope_axes is 3, and this one when it is not.  Errors otherwise as
+ * hermes_append_chunk (EINVAL also for a null or misaligned rope_thw).
+ */
+int hermes_append_chunk_mrope(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                              const void *v, const int32_t *pos, const int32_t *rope_thw,
+                              int32_t n_new, void *out, void *stream);
+
+/*
  * Guidance-prompt scoring (scoring_mode HERMES_SCORE_GUIDANCE; Sec. 3.1
  * deep-layer paragraph and the appendix guidance prompts): n_rows prompt
  * tokens (q, k, v: device bf16, layout as hermes_append_chunk; stacked over
@@ -233,6 +266,14 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
  * rotated by the position change (rotate-half pairs, angles and rotation in
  * fp64, stored as bf16); V is unchanged.
  *
+ * With rope_axes 3 (appendix, 3D M-RoPE re-indexing) each axis is compacted
+ * on its own: a retained entry's t (h, w) coordinate becomes rope_offset +
+ * the number of distinct t (h, w) coordinates the layer retains below it,
+ * so entries that shared a coordinate still share it, and frequency pair j
+ * of its key turns by the change of the coordinate of the section j falls
+ * in (mrope_section).  LAZY fires when the largest retained coordinate on
+ * any axis of any layer + rope_headroom >= rope_limit.
+ *
  * scoring_mode GUIDANCE: W must have been written by hermes_guidance_score
  * this step for every layer whose decision needs it, else ESTATE.
  * Errors: ESTATE, EHIP.
@@ -265,6 +306,11 @@ int hermes_kv_view(const hermes_ctx *ctx, int32_t layer, const void **k, const v
 /* Current RoPE-position buffer of one layer (NULL when the context keeps
  * none); it has the length hermes_kv_view reports. */
 int hermes_kv_view_rope(const hermes_ctx *ctx, int32_t layer, const int32_t **rpos);
+
+/* Current t, h and w coordinate buffers of one layer (rope_axes 3; all NULL
+ * otherwise); they have the length hermes_kv_view reports. */
+int hermes_kv_view_mrope(const hermes_ctx *ctx, int32_t layer, const int32_t **t,
+                         const int32_t **h, const int32_t **w);
 
 /*
  * Layer-dependent budgets from layer weights (Sec. 4 ablation "Layer-

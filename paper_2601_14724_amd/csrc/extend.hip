@@ -11,12 +11,20 @@
 // reindex_decide
 //     the lazy re-indexing trigger (Sec. 3.3): the largest RoPE position any
 //     layer retains after this compression, against the limit.
+// reindex_decide3 / mrope_rank
+//     the same trigger over the t, h and w coordinates, and the per-axis
+//     ranks of 3D M-RoPE re-indexing (appendix, Qwen2.5-VL): on each axis a
+//     retained coordinate becomes offset + the number of distinct retained
+//     coordinates below it (one workgroup per layer and axis, an LDS bitmap
+//     of the coordinates and a prefix of its word popcounts);
 // gather_rope
 //     the order-preserving gather with the summary row inserted at its sorted
 //     place and, when re-indexing applies, every key rotated by the change of
 //     its RoPE position (appendix, 1D re-indexing: p_new = offset + rank,
 //     k_new = k_old * e^{i (p_new - p_old) theta}); layers that did not evict
-//     are re-indexed in place.
+//     are re-indexed in place.  With M-RoPE the frequency pairs of a key are
+//     split into t, h and w sections, and the pairs of each section turn by
+//     the change of that section's coordinate.
 //
 // RoPE layout: rotate-half, channel j pairs with j + d/2 inside each head,
 // theta_j = base^(-2j/d).  Angles, sines, cosines and rotations are fp64; a
@@ -200,6 +208,127 @@ __global__ __launch_bounds__(64) void reindex_decide(DecideArgs a) {
   if (l == 0) a.flag[0] = (r != LLONG_MIN && r + (long long)a.headroom >= (long long)a.limit) ? 1 : 0;
 }
 
+// Lazy trigger with M-RoPE: the largest retained coordinate on any axis of
+// any layer (h and w are not monotone along the cache, so every retained row
+// is read).
+constexpr int RT = 1024;
+__global__ __launch_bounds__(RT) void reindex_decide3(DecideArgs a) {
+  long long r = LLONG_MIN;
+  for (int l = 0; l < a.n_layers; ++l) {
+    const LayerTable &L = a.tab[l];
+    const int c = a.cur[l];
+    const int rows = a.evicts[l] ? a.budget[l] : a.len[l];
+    const int32_t *kept = a.kept + l * a.kept_lstride;
+    for (int i = threadIdx.x; i < rows; i += RT) {
+      const int src = a.evicts[l] ? min(max(kept[i], 0), L.cap - 1) : i;
+      const long long m = max(L.rpos[c][src], max(L.rpos_h[c][src], L.rpos_w[c][src]));
+      r = m > r ? m : r;
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    const long long x = __shfl_xor(r, o);
+    r = x > r ? x : r;
+  }
+  __shared__ long long wm[RT / 64];
+  if ((threadIdx.x & 63) == 0) wm[threadIdx.x >> 6] = r;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int w = 0; w < RT / 64; ++w) r = wm[w] > r ? wm[w] : r;
+    a.flag[0] = (r != LLONG_MIN && r + (long long)a.headroom >= (long long)a.limit) ? 1 : 0;
+  }
+}
+
+// Distinct-rank compaction of one axis of one layer's retained coordinates.
+constexpr int kSpanWords = HERMES_MROPE_MAX_SPAN / 32;
+__global__ __launch_bounds__(RT) void mrope_rank(RankArgs a) {
+  const int jj = blockIdx.x, axis = blockIdx.y;
+  const bool rot = a.reindex == 1 || (a.reindex == 2 && a.flag[0] != 0);
+  if (!rot) return;
+  const int l = a.layer_id[jj];
+  const LayerTable &L = a.tab[l];
+  const int cur = a.cur[jj];
+  const bool inplace = a.mode[jj] != 0;
+  const int rows = a.row_start[jj + 1] - a.row_start[jj];
+  if (rows <= 0) return;
+  const int32_t *C = axis == 0 ? L.rpos[cur] : axis == 1 ? L.rpos_h[cur] : L.rpos_w[cur];
+  const int32_t *kept = a.kept + l * a.kept_lstride;
+  int32_t *out = a.newc + (int64_t)(l * 3 + axis) * a.newc_lstride;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  auto coord = [&](int r) { return C[inplace ? r : min(max(kept[r], 0), L.cap - 1)]; };
+
+  __shared__ uint32_t bits[kSpanWords];
+  __shared__ uint32_t wpre[kSpanWords];
+  __shared__ int red[2][RT / 64];
+  __shared__ uint32_t wsum[RT / 64];
+  // min and max of the retained coordinates
+  int mn = INT_MAX, mx = INT_MIN;
+  for (int r = tid; r < rows; r += RT) {
+    const int c = coord(r);
+    mn = min(mn, c);
+    mx = max(mx, c);
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) {
+    mn = min(mn, __shfl_xor(mn, o));
+    mx = max(mx, __shfl_xor(mx, o));
+  }
+  if (lane == 0) {
+    red[0][wv] = mn;
+    red[1][wv] = mx;
+  }
+  __syncthreads();
+  for (int w = 0; w < RT / 64; ++w) {
+    mn = min(mn, red[0][w]);
+    mx = max(mx, red[1][w]);
+  }
+  const long long span = (long long)mx - (long long)mn + 1;
+  if (span > HERMES_MROPE_MAX_SPAN) {   // wider than the bitmap: coordinates kept
+    for (int r = tid; r < rows; r += RT) out[r] = coord(r);
+    return;
+  }
+  const int nwords = (int)((span + 31) / 32);
+  for (int w = tid; w < nwords; w += RT) bits[w] = 0u;
+  __syncthreads();
+  for (int r = tid; r < rows; r += RT) {
+    const int c = coord(r) - mn;
+    atomicOr(&bits[c >> 5], 1u << (c & 31));
+  }
+  __syncthreads();
+  // exclusive prefix of the word popcounts: thread t owns words [8t, 8t + 8)
+  constexpr int WPT = kSpanWords / RT;
+  uint32_t own = 0;
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int w = tid * WPT + u;
+    own += w < nwords ? (uint32_t)__popc(bits[w]) : 0u;
+  }
+  uint32_t inc = own;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const uint32_t x = __shfl_up(inc, o);
+    if (lane >= o) inc += x;
+  }
+  if (lane == 63) wsum[wv] = inc;
+  __syncthreads();
+  uint32_t base = inc - own;
+  for (int w = 0; w < wv; ++w) base += wsum[w];
+#pragma unroll
+  for (int u = 0; u < WPT; ++u) {
+    const int w = tid * WPT + u;
+    if (w < nwords) {
+      wpre[w] = base;
+      base += (uint32_t)__popc(bits[w]);
+    }
+  }
+  __syncthreads();
+  for (int r = tid; r < rows; r += RT) {
+    const int c = coord(r) - mn;
+    const int w = c >> 5, b = c & 31;
+    out[r] = a.offset + (int)(wpre[w] + (uint32_t)__popc(bits[w] & ((1u << b) - 1u)));
+  }
+}
+
 // ---------------------------------------------------------------------------
 // gather with summary insertion and re-indexing: one wave per output row
 // ---------------------------------------------------------------------------
@@ -225,33 +354,52 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
   int32_t *Pd = L.pos[dst_buf], *Rd = L.rpos[dst_buf];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const double invf = inv_freq(lane % hd, d, a.theta);
+  // M-RoPE: the section (0 = t, 1 = h, 2 = w) of this lane's frequency
+  const bool three = a.axes == 3;
+  const int fj = lane % hd;
+  const int my_axis = fj < a.section[0] ? 0 : fj < a.section[0] + a.section[1] ? 1 : 2;
+  const int32_t *Hs = three ? L.rpos_h[cur] : nullptr, *Ws = three ? L.rpos_w[cur] : nullptr;
+  int32_t *Hd = three ? L.rpos_h[dst_buf] : nullptr, *Wd = three ? L.rpos_w[dst_buf] : nullptr;
+  const int32_t *nc = three ? a.newc + (int64_t)l * 3 * a.newc_lstride : nullptr;
 
   for (int j = blockIdx.x * 4 + wave; j < rows; j += gridDim.x * 4) {
     // source of output row j
     const bool is_sum = has_sum && j == ins;
     const uint16_t *kr, *vr;
-    int p_src, r_src;
+    int p_src, r_src, src_row;
     if (inplace) {
       kr = Ks + (int64_t)j * RE;
       vr = nullptr;
       p_src = Ps[j];
       r_src = Rs[j];
+      src_row = j;
     } else if (is_sum) {
       kr = a.sum_k + (int64_t)l * RE;
       vr = a.sum_v + (int64_t)l * RE;
       p_src = a.sum_meta[4 * l + 1];
       r_src = a.sum_meta[4 * l + 2];
+      src_row = -1;
     } else {
       const int src = min(max(kept[j - (has_sum && j > ins ? 1 : 0)], 0), L.cap - 1);
       kr = Ks + (int64_t)src * RE;
       vr = Vs + (int64_t)src * RE;
       p_src = Ps[src];
       r_src = Rs[src];
+      src_row = src;
     }
-    const int r_new = rot ? a.rope_offset + j : r_src;
-    const int delta = r_new - r_src;
+    int r_new = rot ? a.rope_offset + j : r_src;
+    int delta = r_new - r_src;
+    int h_old = 0, w_old = 0, h_new = 0, w_new = 0;
+    if (three) {   // no summary rows with M-RoPE: src_row >= 0
+      h_old = Hs[src_row];
+      w_old = Ws[src_row];
+      r_new = rot ? nc[j] : r_src;
+      h_new = rot ? nc[a.newc_lstride + j] : h_old;
+      w_new = rot ? nc[2 * a.newc_lstride + j] : w_old;
+      delta = my_axis == 0 ? r_new - r_src : my_axis == 1 ? h_new - h_old : w_new - w_old;
+    }
     uint16_t *kd = Kd + (int64_t)j * RE;
-    if (delta != 0) {
+    if (__any(delta != 0)) {   // uniform over the wave (one row)
       double sn, cs;
       sincos((double)delta * invf, &sn, &cs);
 #pragma unroll
@@ -275,7 +423,13 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
         *reinterpret_cast<uint4 *>(vd + 8 * c) = *reinterpret_cast<const uint4 *>(vr + 8 * c);
       if (lane == 0) Pd[j] = p_src;
     }
-    if (lane == 0) Rd[j] = r_new;
+    if (lane == 0) {
+      Rd[j] = r_new;
+      if (three) {
+        Hd[j] = h_new;
+        Wd[j] = w_new;
+      }
+    }
   }
 }
 
@@ -291,7 +445,13 @@ hipError_t launch_summary(const SummaryArgs &a, int max_T, hipStream_t s) {
 }
 
 hipError_t launch_decide(const DecideArgs &a, hipStream_t s) {
-  hipLaunchKernelGGL(reindex_decide, dim3(1), dim3(64), 0, s, a);
+  if (a.axes == 3) hipLaunchKernelGGL(reindex_decide3, dim3(1), dim3(RT), 0, s, a);
+  else hipLaunchKernelGGL(reindex_decide, dim3(1), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_mrope_rank(const RankArgs &a, hipStream_t s) {
+  hipLaunchKernelGGL(mrope_rank, dim3(a.n_list, 3), dim3(RT), 0, s, a);
   return hipGetLastError();
 }
 

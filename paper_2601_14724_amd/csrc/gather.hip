@@ -30,6 +30,10 @@ __global__ __launch_bounds__(NT) void append_rows(AppendArgs a) {
   for (int e = blockIdx.x * NT + threadIdx.x; e < a.C; e += gridDim.x * NT) {
     L.pos[cur][T0 + e] = a.pos[e];
     if (L.rpos[cur] != nullptr) L.rpos[cur][T0 + e] = a.rope_pos != nullptr ? a.rope_pos[e] : a.pos[e];
+    if (L.rpos_h[cur] != nullptr) {   // M-RoPE: h and w beside t
+      L.rpos_h[cur][T0 + e] = a.rope_h[e];
+      L.rpos_w[cur][T0 + e] = a.rope_w[e];
+    }
   }
 }
 
@@ -59,6 +63,10 @@ __global__ __launch_bounds__(NT) void gather_rows(GatherArgs a) {
     if (c == 0) {
       L.pos[cur ^ 1][row] = L.pos[cur][src];
       if (L.rpos[cur] != nullptr) L.rpos[cur ^ 1][row] = L.rpos[cur][src];
+      if (L.rpos_h[cur] != nullptr) {
+        L.rpos_h[cur ^ 1][row] = L.rpos_h[cur][src];
+        L.rpos_w[cur ^ 1][row] = L.rpos_w[cur][src];
+      }
     }
   }
 }

@@ -23,8 +23,9 @@ size_t round_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
 bool aligned(const void *p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
 
 struct Layout {
-  size_t tab, lse, keys, kept, normpart, wpart, spart, sumk, sumv, smeta, flag, opart, mlpart, total;
-  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride, normpart_lstride;
+  size_t tab, lse, keys, kept, normpart, newc, wpart, spart, sumk, sumv, smeta, flag, opart, mlpart, total;
+  int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride, normpart_lstride,
+      newc_lstride;
   int32_t part_rows;
 };
 
@@ -64,8 +65,17 @@ int check_config(const hermes_config *c) {
     return HERMES_EINVAL;
   if (c->rope_offset < 0 || c->rope_limit < 0 || c->rope_headroom < 0) return HERMES_EINVAL;
   if (!std::isfinite(c->rope_theta)) return HERMES_EINVAL;
+  if (c->rope_axes != 0 && c->rope_axes != 1 && c->rope_axes != 3) return HERMES_EINVAL;
+  if (c->rope_axes == 3) {
+    if (c->summary_mode) return HERMES_ENOTSUP;   // summary tokens carry one RoPE position
+    const int *sec = c->mrope_section;
+    if (sec[0] != 0 || sec[1] != 0 || sec[2] != 0) {
+      if (sec[0] < 0 || sec[1] < 0 || sec[2] < 0) return HERMES_EINVAL;
+      if (sec[0] + sec[1] + sec[2] != c->head_dim / 2) return HERMES_EINVAL;
+    }
+  }
   // The RoPE kernels give each lane one frequency and at most 8 rotate pairs.
-  if ((c->summary_mode || c->reindex_mode) && c->n_kv_heads * c->head_dim > 1024)
+  if ((c->summary_mode || c->reindex_mode || c->rope_axes == 3) && c->n_kv_heads * c->head_dim > 1024)
     return HERMES_ENOTSUP;
   return HERMES_OK;
 }
@@ -88,6 +98,10 @@ Layout layout_of(const hermes_config *c) {
   s.normpart_lstride = (c->max_cap + kNormBlock - 1) / kNormBlock;
   s.normpart = off;
   off = round_up(off + sizeof(double) * (size_t)s.normpart_lstride * c->n_layers);
+  // M-RoPE: re-indexed (t, h, w) of every output row
+  s.newc_lstride = c->rope_axes == 3 ? c->max_cap : 0;
+  s.newc = off;
+  off = round_up(off + sizeof(int32_t) * 3 * (size_t)s.newc_lstride * c->n_layers);
   s.wpart_lstride = (int64_t)c->n_kv_heads * c->max_cap;
   s.wpart = off;
   off = round_up(off + sizeof(double) * (size_t)s.wpart_lstride * c->n_layers);
@@ -155,6 +169,8 @@ struct hermes_ctx {
   int summary_mode, reindex_mode, scoring_mode;
   int rope_offset, rope_limit, rope_headroom;
   double rope_theta;
+  int rope_axes = 1;
+  int section[3] = {0, 0, 0};       // M-RoPE frequency pairs of t, h, w
   bool keep_rpos = false;
   std::vector<int32_t> guided;      // prompt rows of this step's guidance score (0 = none)
   std::vector<int32_t> budget;
@@ -254,9 +270,15 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
     if (b.cap < 1 || b.init_len < 0) return HERMES_EINVAL;
     if (b.cap > cfg->max_cap || b.init_len > b.cap || cfg->budget[l] > b.cap)
       return HERMES_ECAPACITY;
-    if (cfg->summary_mode || cfg->reindex_mode) {
+    if (cfg->summary_mode || cfg->reindex_mode || cfg->rope_axes == 3) {
       for (int p = 0; p < 2; ++p)
         if (b.rpos[p] == nullptr || !aligned(b.rpos[p], 4)) return HERMES_EINVAL;
+    }
+    if (cfg->rope_axes == 3) {
+      for (int p = 0; p < 2; ++p)
+        if (b.rpos_h[p] == nullptr || b.rpos_w[p] == nullptr || !aligned(b.rpos_h[p], 4) ||
+            !aligned(b.rpos_w[p], 4))
+          return HERMES_EINVAL;
     }
   }
   if (cfg->summary_mode) {
@@ -287,7 +309,19 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
   c->rope_limit = cfg->rope_limit;
   c->rope_headroom = cfg->rope_headroom;
   c->rope_theta = cfg->rope_theta > 0.0 ? cfg->rope_theta : 1.0e6;
-  c->keep_rpos = cfg->summary_mode != 0 || cfg->reindex_mode != 0;
+  c->rope_axes = cfg->rope_axes == 3 ? 3 : 1;
+  if (c->rope_axes == 3) {
+    const int half = cfg->head_dim / 2;
+    const int *sec = cfg->mrope_section;
+    if (sec[0] == 0 && sec[1] == 0 && sec[2] == 0) {
+      c->section[0] = half / 4;
+      c->section[1] = (half - half / 4) / 2;
+      c->section[2] = half - c->section[0] - c->section[1];
+    } else {
+      for (int a = 0; a < 3; ++a) c->section[a] = sec[a];
+    }
+  }
+  c->keep_rpos = cfg->summary_mode != 0 || cfg->reindex_mode != 0 || c->rope_axes == 3;
   c->guided.assign(L, 0);
   c->budget.assign(cfg->budget, cfg->budget + L);
   c->cls = cfg->layer_class ? std::vector<int8_t>(cfg->layer_class, cfg->layer_class + L)
@@ -329,6 +363,8 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
       t.v[p] = static_cast<uint16_t *>(layers[l].v[p]);
       t.pos[p] = layers[l].pos[p];
       t.rpos[p] = c->keep_rpos ? layers[l].rpos[p] : nullptr;
+      t.rpos_h[p] = c->rope_axes == 3 ? layers[l].rpos_h[p] : nullptr;
+      t.rpos_w[p] = c->rope_axes == 3 ? layers[l].rpos_w[p] : nullptr;
     }
     t.w = layers[l].w;
     t.s_dbg = layers[l].s_dbg;
@@ -395,6 +431,19 @@ int hermes_kv_view_rope(const hermes_ctx *ctx, int32_t layer, const int32_t **rp
   return HERMES_OK;
 }
 
+int hermes_kv_view_mrope(const hermes_ctx *ctx, int32_t layer, const int32_t **t,
+                         const int32_t **h, const int32_t **w) {
+  if (ctx == nullptr || layer < 0 || layer >= ctx->L || t == nullptr || h == nullptr ||
+      w == nullptr)
+    return HERMES_EINVAL;
+  const bool three = ctx->rope_axes == 3;
+  const int p = ctx->cur[layer];
+  *t = three ? ctx->bufs[layer].rpos[p] : nullptr;
+  *h = three ? ctx->bufs[layer].rpos_h[p] : nullptr;
+  *w = three ? ctx->bufs[layer].rpos_w[p] : nullptr;
+  return HERMES_OK;
+}
+
 int hermes_budget_from_weights(const double *weights, int32_t n_layers, int64_t total,
                                int32_t *budget) {
   if (weights == nullptr || budget == nullptr || n_layers < 1 || total < n_layers)
@@ -419,10 +468,13 @@ int hermes_budget_from_weights(const double *weights, int32_t n_layers, int64_t 
 }
 
 static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
-                       const void *v, const int32_t *pos, const int32_t *rope_pos, int32_t n_new,
-                       void *out, void *stream) {
+                       const void *v, const int32_t *pos, const int32_t *rope_pos,
+                       const int32_t *rope_thw, int32_t n_new, void *out, void *stream) {
   if (ctx == nullptr) return HERMES_EINVAL;
   if (ctx->poisoned) return HERMES_ESTATE;
+  // M-RoPE contexts take their chunks with (t, h, w) coordinates only
+  if ((ctx->rope_axes == 3) != (rope_thw != nullptr)) return HERMES_ESTATE;
+  if (!aligned(rope_thw, 4)) return HERMES_EINVAL;
   const int L = ctx->L;
   if (layer != HERMES_ALL_LAYERS && (layer < 0 || layer >= L)) return HERMES_EINVAL;
   if (q == nullptr || k == nullptr || v == nullptr || pos == nullptr || out == nullptr)
@@ -468,7 +520,9 @@ static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void
   ap.kn = static_cast<const uint16_t *>(k);
   ap.vn = static_cast<const uint16_t *>(v);
   ap.pos = pos;
-  ap.rope_pos = rope_pos;
+  ap.rope_pos = rope_thw != nullptr ? rope_thw : rope_pos;
+  ap.rope_h = rope_thw != nullptr ? rope_thw + n_new : nullptr;
+  ap.rope_w = rope_thw != nullptr ? rope_thw + 2 * n_new : nullptr;
   ap.kv_lstride = kv_ls;
   ap.row_elems = ctx->Hkv * ctx->D;
   ap.C = n_new;
@@ -550,13 +604,22 @@ static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void
 int hermes_append_chunk(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
                         const void *v, const int32_t *pos, int32_t n_new, void *out,
                         void *stream) {
-  return append_impl(ctx, layer, q, k, v, pos, nullptr, n_new, out, stream);
+  return append_impl(ctx, layer, q, k, v, pos, nullptr, nullptr, n_new, out, stream);
 }
 
 int hermes_append_chunk_at(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
                            const void *v, const int32_t *pos, const int32_t *rope_pos,
                            int32_t n_new, void *out, void *stream) {
-  return append_impl(ctx, layer, q, k, v, pos, rope_pos, n_new, out, stream);
+  return append_impl(ctx, layer, q, k, v, pos, rope_pos, nullptr, n_new, out, stream);
+}
+
+int hermes_append_chunk_mrope(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
+                              const void *v, const int32_t *pos, const int32_t *rope_thw,
+                              int32_t n_new, void *out, void *stream) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  if (ctx->rope_axes != 3) return HERMES_ESTATE;
+  if (rope_thw == nullptr) return HERMES_EINVAL;
+  return append_impl(ctx, layer, q, k, v, pos, nullptr, rope_thw, n_new, out, stream);
 }
 
 int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const void *k,
@@ -765,6 +828,10 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
     ga.sum_k = reinterpret_cast<const uint16_t *>(ctx->ws + ctx->lay.sumk);
     ga.sum_v = reinterpret_cast<const uint16_t *>(ctx->ws + ctx->lay.sumv);
     ga.sum_meta = meta;
+    ga.axes = ctx->rope_axes;
+    for (int a = 0; a < 3; ++a) ga.section[a] = ctx->section[a];
+    ga.newc = reinterpret_cast<const int32_t *>(ctx->ws + ctx->lay.newc);
+    ga.newc_lstride = ctx->lay.newc_lstride;
     if (ctx->reindex_mode == HERMES_REINDEX_LAZY) {
       DecideArgs da;
       std::memset(&da, 0, sizeof(da));
@@ -776,6 +843,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
       da.n_layers = L;
       da.limit = ctx->rope_limit;
       da.headroom = ctx->rope_headroom;
+      da.axes = ctx->rope_axes;
       for (int l = 0; l < L; ++l) {
         da.len[l] = ctx->len[l];
         da.budget[l] = ctx->budget[l];
@@ -784,6 +852,27 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
         da.has_sum[l] = has_sum[l];
       }
       rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_decide(da, s); });
+      if (rc != HERMES_OK) return rc;
+    }
+    if (n > 0 && ctx->rope_axes == 3 && ctx->reindex_mode != HERMES_REINDEX_NONE) {
+      RankArgs ra;
+      std::memset(&ra, 0, sizeof(ra));
+      ra.tab = ctx->d_tab;
+      ra.kept = sa.kept;
+      ra.kept_lstride = sa.kept_lstride;
+      ra.newc = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.newc);
+      ra.newc_lstride = ctx->lay.newc_lstride;
+      ra.flag = flag;
+      ra.reindex = ga.reindex;
+      ra.offset = ctx->rope_offset;
+      ra.n_list = n;
+      for (int j = 0; j < n; ++j) {
+        ra.layer_id[j] = ga.layer_id[j];
+        ra.cur[j] = ga.cur[j];
+        ra.mode[j] = ga.mode[j];
+        ra.row_start[j + 1] = ga.row_start[j + 1];
+      }
+      rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_mrope_rank(ra, s); });
       if (rc != HERMES_OK) return rc;
     }
     if (n > 0) {

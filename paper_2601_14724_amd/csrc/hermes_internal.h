@@ -16,7 +16,9 @@ struct LayerTable {
   uint16_t *k[2];
   uint16_t *v[2];
   int32_t *pos[2];
-  int32_t *rpos[2];         // RoPE positions of the stored keys (null when not kept)
+  int32_t *rpos[2];         // RoPE positions of the stored keys (null when not kept); t with M-RoPE
+  int32_t *rpos_h[2];       // M-RoPE h and w coordinates (null unless three axes)
+  int32_t *rpos_w[2];
   float *w;
   float *s_dbg;
   int32_t *kept_dbg;
@@ -113,6 +115,10 @@ struct GatherArgs {
   const int32_t *flag;      // lazy re-indexing decision (device)
   const uint16_t *sum_k, *sum_v;   // [n_layers][row_elems] staged summary rows
   const int32_t *sum_meta;  // [n_layers][4]: insert index, stream pos, RoPE pos, evicted
+  int32_t axes;             // 1, or 3 for M-RoPE (t, h, w)
+  int32_t section[3];       // M-RoPE: frequency pairs of the t, h, w sections
+  const int32_t *newc;      // M-RoPE: [n_layers][3][newc_lstride] re-indexed coordinates by output row
+  int64_t newc_lstride;
   int32_t row_start[kMaxLayers + 1];   // prefix of output rows over the list
   int8_t layer_id[kMaxLayers];
   int8_t cur[kMaxLayers];
@@ -147,11 +153,32 @@ struct DecideArgs {
   const int32_t *sum_meta;
   int32_t *flag;
   int32_t n_layers, limit, headroom;
+  int32_t axes;             // 3: the largest of the t, h and w coordinates
   int32_t len[kMaxLayers];      // by layer: T before compression
   int32_t budget[kMaxLayers];
   int8_t cur[kMaxLayers];
   int8_t evicts[kMaxLayers];
   int8_t has_sum[kMaxLayers];
+};
+
+// M-RoPE ranks (appendix, 3D re-indexing): for list entry j and axis a, the
+// coordinate of every output row (mode 0: kept row kept[r] of the current
+// buffer; mode 1: row r in place) becomes offset + the number of distinct
+// retained coordinates below it, written to newc[layer][a][r].
+struct RankArgs {
+  const LayerTable *tab;
+  const int32_t *kept;
+  int64_t kept_lstride;
+  int32_t *newc;
+  int64_t newc_lstride;
+  const int32_t *flag;      // lazy decision (device)
+  int32_t reindex;          // 0 never, 1 always, 2 when *flag != 0
+  int32_t offset;
+  int32_t n_list;
+  int32_t row_start[kMaxLayers + 1];
+  int8_t layer_id[kMaxLayers];
+  int8_t cur[kMaxLayers];
+  int8_t mode[kMaxLayers];
 };
 
 // Append copy: new K/V rows and positions into rows [T0, T0 + C) of the
@@ -160,7 +187,8 @@ struct AppendArgs {
   const LayerTable *tab;
   const uint16_t *kn, *vn;
   const int32_t *pos;
-  const int32_t *rope_pos;  // RoPE positions of the new rows (null: = pos)
+  const int32_t *rope_pos;  // RoPE positions of the new rows (null: = pos); t with M-RoPE
+  const int32_t *rope_h, *rope_w;   // M-RoPE h and w of the new rows (null unless three axes)
   int64_t kv_lstride;
   int32_t row_elems, C, n_list;
   int32_t T0[kMaxLayers];
@@ -181,6 +209,7 @@ hipError_t launch_topk(const float *keys, int n, int k, int32_t *out, hipStream_
 hipError_t launch_summary(const SummaryArgs &a, int max_T, hipStream_t s);
 hipError_t launch_decide(const DecideArgs &a, hipStream_t s);
 hipError_t launch_gather_rope(const GatherArgs &a, hipStream_t s);
+hipError_t launch_mrope_rank(const RankArgs &a, hipStream_t s);
 
 // Geometry shared by host sizing and kernels.
 constexpr int kAttnRowsPerBlock = 128;   // packed (row, head) pairs per workgroup

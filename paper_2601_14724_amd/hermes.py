@@ -31,7 +31,8 @@ SCORE_CHUNK, SCORE_GUIDANCE = 0, 1
 
 EXPORTED = ("hermes_workspace_bytes", "hermes_kv_init", "hermes_append_chunk",
             "hermes_append_chunk_at", "hermes_guidance_score", "hermes_compress",
-            "hermes_query_attend", "hermes_kv_rewind", "hermes_kv_view", "hermes_kv_view_rope",
+            "hermes_append_chunk_mrope", "hermes_query_attend", "hermes_kv_rewind",
+            "hermes_kv_view", "hermes_kv_view_rope", "hermes_kv_view_mrope",
             "hermes_budget_from_weights", "hermes_kv_destroy", "hermes_strerror",
             "hermes_select_topk", "hermes_profile_enable", "hermes_profile_read")
 
@@ -50,7 +51,8 @@ class HermesConfig(ctypes.Structure):
                 ("summary_mode", ctypes.c_int32), ("reindex_mode", ctypes.c_int32),
                 ("rope_offset", ctypes.c_int32), ("rope_limit", ctypes.c_int32),
                 ("rope_headroom", ctypes.c_int32), ("rope_theta", ctypes.c_double),
-                ("scoring_mode", ctypes.c_int32)]
+                ("scoring_mode", ctypes.c_int32), ("rope_axes", ctypes.c_int32),
+                ("mrope_section", ctypes.c_int32 * 3)]
 
 
 class LayerBuffers(ctypes.Structure):
@@ -58,7 +60,8 @@ class LayerBuffers(ctypes.Structure):
                 ("pos", ctypes.c_void_p * 2), ("w", ctypes.c_void_p),
                 ("s_dbg", ctypes.c_void_p), ("kept_dbg", ctypes.c_void_p),
                 ("cap", ctypes.c_int32), ("init_len", ctypes.c_int32),
-                ("rpos", ctypes.c_void_p * 2)]
+                ("rpos", ctypes.c_void_p * 2), ("rpos_h", ctypes.c_void_p * 2),
+                ("rpos_w", ctypes.c_void_p * 2)]
 
 
 _vp, _i32, _i64, _dbl = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
@@ -71,6 +74,11 @@ lib.hermes_append_chunk.restype = ctypes.c_int
 lib.hermes_append_chunk.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
 lib.hermes_append_chunk_at.restype = ctypes.c_int
 lib.hermes_append_chunk_at.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
+lib.hermes_append_chunk_mrope.restype = ctypes.c_int
+lib.hermes_append_chunk_mrope.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
+lib.hermes_kv_view_mrope.restype = ctypes.c_int
+lib.hermes_kv_view_mrope.argtypes = [_vp, _i32, ctypes.POINTER(_vp), ctypes.POINTER(_vp),
+                                     ctypes.POINTER(_vp)]
 lib.hermes_guidance_score.restype = ctypes.c_int
 lib.hermes_guidance_score.argtypes = [_vp, _i32, _vp, _vp, _vp, _i32, _vp]
 lib.hermes_kv_view_rope.restype = ctypes.c_int
@@ -152,7 +160,8 @@ class HermesKV:
     mass, optional debug outputs and the workspace) is allocated here with
     torch; the library only receives pointers.  `init` optionally gives each
     layer's initial (k, v, pos) as device tensors of shapes [n][Hkv][d] bf16,
-    [n][Hkv][d] bf16 and [n] int32.
+    [n][Hkv][d] bf16 and [n] int32, then optionally its RoPE positions [n]
+    (rope_axes 1) or its (t, h, w) coordinates [3][n] int32 (rope_axes 3).
     """
 
     def __init__(self, n_layers: int, n_q_heads: int, n_kv_heads: int, head_dim: int,
@@ -165,14 +174,16 @@ class HermesKV:
                  force_scores: bool = False, debug: bool = False, device: str = "cuda",
                  summary_mode: int = 0, reindex_mode: int = REINDEX_NONE, rope_offset: int = 0,
                  rope_limit: int = 0, rope_headroom: int = 0, rope_theta: float = 1.0e6,
-                 scoring_mode: int = SCORE_CHUNK):
+                 scoring_mode: int = SCORE_CHUNK, rope_axes: int = 1,
+                 mrope_section: Sequence[int] = (0, 0, 0)):
         self.L, self.Hq, self.Hkv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         self.budgets = [int(b) for b in budgets]
         self.max_chunk = int(max_chunk)
         init_lens = [0] * n_layers if init is None else [int(t[0].shape[0]) for t in init]
         if cap is None:
             cap = max(max(init_lens), max(self.budgets) + int(bool(summary_mode))) + self.max_chunk
-        self.keep_rpos = bool(summary_mode) or reindex_mode != REINDEX_NONE
+        self.rope_axes = 3 if rope_axes == 3 else 1
+        self.keep_rpos = bool(summary_mode) or reindex_mode != REINDEX_NONE or self.rope_axes == 3
         self.cap = int(cap)
         self.device = torch.device(device)
         dev = self.device
@@ -185,6 +196,11 @@ class HermesKV:
                     for _ in range(n_layers)]
         self.rpos = ([[torch.zeros(self.cap, dtype=torch.int32, device=dev) for _ in range(2)]
                       for _ in range(n_layers)] if self.keep_rpos else None)
+        three = self.rope_axes == 3
+        self.rpos_h = ([[torch.zeros(self.cap, dtype=torch.int32, device=dev) for _ in range(2)]
+                        for _ in range(n_layers)] if three else None)
+        self.rpos_w = ([[torch.zeros(self.cap, dtype=torch.int32, device=dev) for _ in range(2)]
+                        for _ in range(n_layers)] if three else None)
         self.w = [torch.zeros(self.cap, dtype=torch.float32, device=dev) for _ in range(n_layers)]
         self.s_dbg = ([torch.zeros(self.cap, dtype=torch.float32, device=dev)
                        for _ in range(n_layers)] if debug else None)
@@ -197,7 +213,13 @@ class HermesKV:
                 self.k[l][0][:n].copy_(k0)
                 self.v[l][0][:n].copy_(v0)
                 self.pos[l][0][:n].copy_(p0)
-                if self.keep_rpos:    # RoPE positions (4th element), default the stream ones
+                if three and n > 0:   # (t, h, w) coordinates [3][n] (4th element)
+                    if len(t) < 4:
+                        raise ValueError("rope_axes 3: init needs (k, v, pos, thw)")
+                    self.rpos[l][0][:n].copy_(t[3][0])
+                    self.rpos_h[l][0][:n].copy_(t[3][1])
+                    self.rpos_w[l][0][:n].copy_(t[3][2])
+                elif self.keep_rpos and not three:   # RoPE positions (4th element), default the stream ones
                     self.rpos[l][0][:n].copy_(t[3] if len(t) > 3 else p0)
         self._budget_arr = (ctypes.c_int32 * n_layers)(*self.budgets)
         self._class_arr = ((ctypes.c_int8 * n_layers)(*layer_class)
@@ -218,6 +240,9 @@ class HermesKV:
         cfg.summary_mode, cfg.reindex_mode, cfg.scoring_mode = int(summary_mode), reindex_mode, scoring_mode
         cfg.rope_offset, cfg.rope_limit, cfg.rope_headroom = rope_offset, rope_limit, rope_headroom
         cfg.rope_theta = rope_theta
+        cfg.rope_axes = int(rope_axes)
+        for a in range(3):
+            cfg.mrope_section[a] = int(mrope_section[a])
         self._cfg = cfg
         nbytes = lib.hermes_workspace_bytes(ctypes.byref(cfg))
         if nbytes == 0:
@@ -238,6 +263,10 @@ class HermesKV:
             if self.keep_rpos:
                 for p in range(2):
                     b.rpos[p] = self.rpos[l][p].data_ptr()
+            if three:
+                for p in range(2):
+                    b.rpos_h[p] = self.rpos_h[l][p].data_ptr()
+                    b.rpos_w[p] = self.rpos_w[l][p].data_ptr()
         self._bufs = bufs
         ctx = ctypes.c_void_p()
         check(lib.hermes_kv_init(ctypes.byref(cfg), bufs, self.workspace.data_ptr(), nbytes,
@@ -253,13 +282,20 @@ class HermesKV:
 
     def append(self, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, pos: torch.Tensor,
                layer: int = ALL_LAYERS, out: Optional[torch.Tensor] = None,
-               rope_pos: Optional[torch.Tensor] = None) -> torch.Tensor:
+               rope_pos: Optional[torch.Tensor] = None,
+               rope_thw: Optional[torch.Tensor] = None) -> torch.Tensor:
         n = q.shape[-3]
         self._check_inputs(q, k, v, n, layer)
         _need(pos, torch.int32, (n,), "pos")
         if out is None:
             out = torch.empty_like(q)
-        if rope_pos is None:
+        if rope_thw is not None:
+            _need(rope_thw, torch.int32, (3, n), "rope_thw")
+            check(lib.hermes_append_chunk_mrope(self.ctx, layer, q.data_ptr(), k.data_ptr(),
+                                                v.data_ptr(), pos.data_ptr(), rope_thw.data_ptr(),
+                                                n, out.data_ptr(), _stream()),
+                  "hermes_append_chunk_mrope")
+        elif rope_pos is None:
             check(lib.hermes_append_chunk(self.ctx, layer, q.data_ptr(), k.data_ptr(),
                                           v.data_ptr(), pos.data_ptr(), n, out.data_ptr(),
                                           _stream()), "hermes_append_chunk")
@@ -317,6 +353,18 @@ class HermesKV:
             raise ValueError("this cache keeps no RoPE positions")
         p = 0 if rp.value == self.rpos[layer][0].data_ptr() else 1
         return self.rpos[layer][p][:self.length(layer)]
+
+    def view_mrope(self, layer: int) -> torch.Tensor:
+        """(t, h, w) coordinates [3][len] of the layer's current buffer."""
+        t, h, w = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+        check(lib.hermes_kv_view_mrope(self.ctx, layer, ctypes.byref(t), ctypes.byref(h),
+                                       ctypes.byref(w)), "hermes_kv_view_mrope")
+        if not t.value:
+            raise ValueError("this cache keeps no M-RoPE coordinates")
+        p = 0 if t.value == self.rpos[layer][0].data_ptr() else 1
+        n = self.length(layer)
+        return torch.stack([self.rpos[layer][p][:n], self.rpos_h[layer][p][:n],
+                            self.rpos_w[layer][p][:n]])
 
     # -------------------------------------------------------------- profiling
     def profile(self, on: bool = True) -> None:

@@ -25,8 +25,13 @@ def make_cache(wl: wk.Workload, device="cuda", max_chunk: Optional[int] = None,
     """A HermesKV holding every layer's initial cache of `wl`."""
     if caches is None:
         caches = [wk.gen_cache(wl, l) for l in range(wl.n_layers)]
-    init = [(bf16_tensor(c["k"], device), bf16_tensor(c["v"], device),
-             torch.from_numpy(c["pos"]).to(device)) for c in caches]
+    init = []
+    for c in caches:
+        t = (bf16_tensor(c["k"], device), bf16_tensor(c["v"], device),
+             torch.from_numpy(c["pos"]).to(device))
+        if "thw" in c:        # M-RoPE (t, h, w) coordinates [3][n]
+            t = t + (torch.from_numpy(np.ascontiguousarray(c["thw"], dtype=np.int32)).to(device),)
+        init.append(t)
     mc = max_chunk if max_chunk is not None else max(wl.chunk, wl.query_len)
     return HermesKV(wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.budgets, mc,
                     cap=cap if cap is not None else wl.cap(), init=init, device=device, **kw)

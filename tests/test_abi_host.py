@@ -214,3 +214,38 @@ def test_budget_from_weights_rejects(weights, total):
     with pytest.raises(H.HermesError) as e:
         H.budget_from_weights(weights, total)
     assert e.value.code == H.EINVAL
+
+
+def _sec(a, b, c):
+    return (ctypes.c_int32 * 3)(a, b, c)
+
+
+@pytest.mark.parametrize("over,code", [
+    ({"rope_axes": 2}, H.EINVAL),
+    ({"rope_axes": -1}, H.EINVAL),
+    ({"rope_axes": 3, "summary_mode": 1}, H.ENOTSUP),
+    ({"rope_axes": 3, "mrope_section": _sec(8, 8, 8)}, H.EINVAL),      # sums to 24, not d/2 = 32
+    ({"rope_axes": 3, "mrope_section": _sec(-1, 17, 16)}, H.EINVAL),
+    ({"rope_axes": 3, "n_q_heads": 16, "n_kv_heads": 16, "head_dim": 128}, H.ENOTSUP),
+])
+def test_init_rejects_bad_mrope_config(over, code):
+    rc, ctx = _init(_cfg(**over), _bufs(3), nbytes=1 << 30)
+    assert rc == code and not ctx.value
+
+
+def test_mrope_needs_all_three_coordinate_buffers():
+    b = _bufs(3)
+    for l in range(3):
+        b[l].rpos[0] = b[l].rpos[1] = FAKE
+    assert _init(_cfg(rope_axes=3), b)[0] == H.EINVAL          # no h / w buffers
+    for l in range(3):
+        b[l].rpos_h[0] = b[l].rpos_h[1] = FAKE
+        b[l].rpos_w[0] = FAKE
+        b[l].rpos_w[1] = FAKE + 2                                # misaligned
+    assert _init(_cfg(rope_axes=3), b)[0] == H.EINVAL
+
+
+def test_workspace_grows_with_mrope_coordinates():
+    base = H.lib.hermes_workspace_bytes(ctypes.byref(_cfg(max_cap=4096)))
+    three = H.lib.hermes_workspace_bytes(ctypes.byref(_cfg(max_cap=4096, rope_axes=3)))
+    assert three - base >= 3 * 3 * 4096 * 4        # (t, h, w) of every row of 3 layers

@@ -304,3 +304,73 @@ def test_fullsize_7b_summary_and_eager_reindex():
     for l in range(wl.n_layers):
         _cmp_layer(l, kv, compact[l], "c3")
     kv.close()
+
+
+# ------------------------------------------------------------- 3D M-RoPE
+
+def _grid(n, H, W, offset, t_step):
+    """(t, h, w) [n][3] of tokens laid out frame by frame, row by row."""
+    s = np.arange(n)
+    f, r = s // (H * W), s % (H * W)
+    return np.stack([offset + f * t_step, offset + r // W, offset + r % W], 1).astype(np.int64)
+
+
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128)])
+@pytest.mark.parametrize("mode", ["eager", "lazy_fires", "lazy_waits"])
+def test_mrope_reindex(shape, mode):
+    """5 cached frames of 14 x 14 tokens (t step 2, text prefix 3) + 1 new
+    frame; the last layer keeps everything and is re-indexed in place."""
+    Hq, Hkv, d = shape
+    classes = [S, M, D, D]
+    T0, C = 5 * 196, 196
+    wl = _wl("ext_mrope", 60 + d, 4, Hq, Hkv, d, T0, C, (500, 600, 700, 1200))
+    caches = [wk.gen_cache(wl, l) for l in range(4)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(4)]
+    g = _grid(T0 + C, 14, 14, offset=3, t_step=2)
+    for c in caches:
+        c["thw"] = g[:T0].T.copy()
+    section = (8, 12, 12) if d == 64 else (16, 24, 24)
+    # the largest coordinate retained anywhere is h = w = 3 + 13 = 16 (t reaches 13)
+    limit = {"eager": 0, "lazy_fires": 18, "lazy_waits": 19}[mode]
+    ext = he.ExtConfig(reindex_mode=he.REINDEX_EAGER if mode == "eager" else he.REINDEX_LAZY,
+                       rope_offset=5, rope_limit=limit, rope_headroom=2, rope_axes=3,
+                       mrope_section=section)
+    say(f"mrope {shape} {mode}")
+    ext_caches = [he.ExtLayerCache(f64(c["k"]), f64(c["v"]), c["pos"].astype(np.int64),
+                                   g[:T0, 0].copy(), g[:T0].copy()) for c in caches]
+    ext_chunks = [dict(ch, rope_thw=g[T0:].T.copy()) for ch in _ext_chunks(chunks)]
+    ref = he.stream_step_ext(ext_caches, ext_chunks, orc.OracleConfig(budgets=list(wl.budgets),
+                                                                      classes=classes), ext)
+    assert ref["reindexed"] == (mode != "lazy_waits")
+    kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, layer_class=classes,
+                              reindex_mode=ext.reindex_mode, rope_offset=5, rope_limit=limit,
+                              rope_headroom=2, rope_axes=3, mrope_section=section)
+    t = streaming.chunk_tensors(_stack(chunks), "cuda")
+    thw = torch.from_numpy(np.ascontiguousarray(g[T0:].T, dtype=np.int32)).cuda()
+    kv.append(t["q"], t["k"], t["v"], t["pos"], rope_thw=thw)
+    kv.compress()
+    torch.cuda.synchronize()
+    compact, reidx = _check_step(wl, classes, ext, kv, ref, f"mrope {mode}")
+    assert reidx == ref["reindexed"]
+    for l in range(4):
+        got = kv.view_mrope(l).cpu().numpy().T
+        assert np.array_equal(got, compact[l].rpos3), f"layer {l}: coordinates differ"
+    kv.close()
+
+
+def test_mrope_append_entry_points_follow_the_context():
+    wl = _wl("ext_mrope_state", 70, 2, 4, 2, 64, 0, 8, (64, 64))
+    caches = [wk.gen_cache(wl, l) for l in range(2)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(2)]
+    t = streaming.chunk_tensors(_stack(chunks), "cuda")
+    thw = torch.zeros((3, 8), dtype=torch.int32, device="cuda")
+    three = streaming.make_cache(wl, device="cuda", caches=caches, rope_axes=3)
+    with pytest.raises(H.HermesError) as e:
+        three.append(t["q"], t["k"], t["v"], t["pos"])
+    assert e.value.code == H.ESTATE
+    three.close()
+    one = streaming.make_cache(wl, device="cuda", caches=caches)
+    with pytest.raises(H.HermesError) as e:
+        one.append(t["q"], t["k"], t["v"], t["pos"], rope_thw=thw)
+    assert e.value.code == H.ESTATE
+    one.close()
