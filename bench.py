@@ -337,7 +337,8 @@ def extension_bench(wl, caches, t, steps: int, warmup: int, prompt_rows: int = 6
     """The adjacent rows on the same workload: (a) summary tokens in the deep
     layers plus eager RoPE re-indexing at every compression, (b) W from a
     guidance prompt of `prompt_rows` tokens per non-shallow layer instead of
-    the chunk.  Reports step time and per-kernel averages."""
+    the chunk, (c) eager 3D M-RoPE re-indexing.  Reports step time and
+    per-kernel averages."""
     import torch
 
     from paper_2601_14724_amd import hermes as H
@@ -395,6 +396,26 @@ def extension_bench(wl, caches, t, steps: int, warmup: int, prompt_rows: int = 6
     dt, ks = timed(kv, step_b)
     out["guidance_prompt"] = {"ms_per_step": round(dt * 1e3, 4), "prompt_rows": prompt_rows,
                               "kernels_ms": ks}
+    kv.close()
+    del kv
+
+    # (c) 3D M-RoPE: frames of 14 x 14 tokens (t step 2, text prefix 14),
+    # every axis left-compacted and every key turned at every compression
+    n0 = wl.init_len
+    s = np.arange(n0 + wl.chunk)
+    fr, r = s // 196, s % 196
+    grid = np.stack([14 + 2 * fr, 14 + r // 14, 14 + r % 14]).astype(np.int32)   # [3][n]
+    caches3 = [dict(c, thw=grid[:, :n0]) for c in caches]
+    kv = streaming.make_cache(wl, device=dev, caches=caches3, reindex_mode=H.REINDEX_EAGER,
+                              rope_offset=14, rope_axes=3)
+    thw = torch.from_numpy(np.ascontiguousarray(grid[:, n0:])).to(dev)
+
+    def step_c():
+        kv.rewind()
+        kv.append(t["q"], t["k"], t["v"], t["pos"], out=o, rope_thw=thw)
+        kv.compress()
+    dt, ks = timed(kv, step_c)
+    out["mrope_eager_reindex"] = {"ms_per_step": round(dt * 1e3, 4), "kernels_ms": ks}
     kv.close()
     return out
 
