@@ -425,7 +425,8 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   const int k0 = kblk * BK;
   if (k0 >= T) return;
 
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  // wave index made scalar: the loop bounds below derive from it and stay uniform
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   const int half = lane >> 5, l32 = lane & 31;
   // Each wave owns 64 candidates (two MFMA column blocks of 32).
   const int kw0 = k0 + wave * 64;
@@ -458,36 +459,38 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   uint4 qreg[NLD];
   float lreg = INFINITY;
   auto tile_p = [&](int it) { return p_begin + it * BQS; };
-  // Tiles are loaded in order, so each thread's packed rows p = (r, g) step
-  // by BQS per tile without a division by G.
-  int ld_p[NLD], ld_r[NLD], ld_g[NLD];
+  // Tiles are loaded in order, so each thread's packed row p = (r, g) steps
+  // by BQS per tile: r by BQS / G and g by BQS % G, plus one row when g wraps
+  // past G; its address moves by the matching fixed amounts.
+  int ld_p[NLD], ld_g[NLD];
+  const uint16_t *ld_q[NLD];
   const int step_r = BQS / G, step_g = BQS - (BQS / G) * G;
+  const int64_t dstep = (int64_t)(step_r * Hq + step_g) * D, dwrap = (int64_t)(Hq - G) * D;
 #pragma unroll
   for (int u = 0; u < NLD; ++u) {
     ld_p[u] = p_begin + (tid + u * 256) / CH;
-    ld_r[u] = ld_p[u] / G;
-    ld_g[u] = ld_p[u] - ld_r[u] * G;
+    const int r0 = ld_p[u] / G;
+    ld_g[u] = ld_p[u] - r0 * G;
+    ld_q[u] = q + ((int64_t)r0 * Hq + kv_blk * G + ld_g[u]) * D + ((tid + u * 256) % CH) * 8;
   }
-  auto load_tile = [&](int it) {
+  // FULL: every row of the tile is < P (no bounds test on the loads)
+  auto load_tile = [&](int it, auto full) {
     const int pt = tile_p(it);
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      const int e = tid + u * 256;
       uint4 v = {0u, 0u, 0u, 0u};
-      if (ld_p[u] < P) v = gload16(q + ((int64_t)ld_r[u] * Hq + kv_blk * G + ld_g[u]) * D + (e % CH) * 8);
+      if (decltype(full)::value || ld_p[u] < P) v = gload16(ld_q[u]);
       qreg[u] = v;
       ld_p[u] += BQS;
-      ld_r[u] += step_r;
       ld_g[u] += step_g;
-      if (ld_g[u] >= G) {
-        ld_g[u] -= G;
-        ++ld_r[u];
-      }
+      const bool wrap = ld_g[u] >= G;
+      ld_g[u] -= wrap ? G : 0;
+      ld_q[u] += dstep + (wrap ? dwrap : 0);
     }
-    if (tid < BQS) lreg = (pt + tid < P) ? lse_l[(int64_t)kv_blk * P + pt + tid] : INFINITY;
+    if (tid < BQS)
+      lreg = (decltype(full)::value || pt + tid < P) ? lse_l[(int64_t)kv_blk * P + pt + tid] : INFINITY;
   };
-  auto store_tile = [&](int it) {
-    const int b = it % 3;
+  auto store_tile = [&](int b) {
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
       const int e = tid + u * 256;
@@ -507,8 +510,7 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
       kf[kb][kk] = ok ? __builtin_bit_cast(bf16x8, gload16(krow + 16 * kk + 8 * half)) : bf16x8{};
   }
   // S = Q K^T for one 32-row tile: lane = candidate, register = query row.
-  auto scores = [&](int it, f32x16 *s) {
-    const int b = it % 3;
+  auto scores = [&](int b, f32x16 *s) {
     s[0] = f32x16{};
     s[1] = f32x16{};
 #pragma unroll
@@ -519,8 +521,7 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
     }
   };
   double wacc[2] = {0.0, 0.0};
-  auto read_lse = [&](int it, float *lv) {
-    const int b = it % 3;
+  auto read_lse = [&](int b, float *lv) {
 #pragma unroll
     for (int grp = 0; grp < 4; ++grp) {
       const float4 l4 = *reinterpret_cast<const float4 *>(&Ls[b][8 * grp + 4 * half]);
@@ -547,9 +548,10 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   auto acc_plain = [&](const f32x16 *s, const float *lv) {
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
-      float t0 = 0.f, t1 = 0.f;
+      float t0 = fast_exp2(fmaf(s[kb][0], c, -lv[0]));
+      float t1 = fast_exp2(fmaf(s[kb][1], c, -lv[1]));
 #pragma unroll
-      for (int e = 0; e < 16; e += 2) {
+      for (int e = 2; e < 16; e += 2) {
         t0 += fast_exp2(fmaf(s[kb][e], c, -lv[e]));
         t1 += fast_exp2(fmaf(s[kb][e + 1], c, -lv[e + 1]));
       }
@@ -559,13 +561,17 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   // tiles [0, n_mask) touch the causal edge of this wave's candidates
   const int n_mask = min(nit, max(0, (pmask_end - p_begin + BQS - 1) / BQS));
 
-  load_tile(0);
+  using Full = std::integral_constant<bool, true>;
+  using Edge = std::integral_constant<bool, false>;
+  // tiles [0, nfull) lie wholly below P
+  const int nfull = (P - p_begin) / BQS;
+  load_tile(0, Edge{});
   store_tile(0);
   if (nit > 1) {
-    load_tile(1);
+    load_tile(1, Edge{});
     store_tile(1);
   }
-  if (nit > 2) load_tile(2);
+  if (nit > 2) load_tile(2, Edge{});
   __syncthreads();
   // One tile per trip, scores then probabilities: without a second score
   // buffer the kernel fits three waves per SIMD, which hide the MFMA and LDS
@@ -573,25 +579,25 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   f32x16 s_cur[2];
   auto step = [&](int it, auto masked) {
     float lv[16];
-    scores(it, s_cur);
-    read_lse(it, lv);
+    scores(it % 3, s_cur);
+    read_lse(it % 3, lv);
     if constexpr (decltype(masked)::value) acc_masked(it, s_cur, lv); else acc_plain(s_cur, lv);
     if (it + 2 < nit) {
-      store_tile(it + 2);
-      if (it + 3 < nit) load_tile(it + 3);
+      store_tile((it + 2) % 3);
+      if (it + 3 < nit) load_tile(it + 3, Edge{});
     }
     __syncthreads();
   };
   int it = 0;
   for (; it < n_mask; ++it) step(it, std::integral_constant<bool, true>{});
   // steady state: no branches inside the body
-  for (; it + 3 < nit; ++it) {
+  for (; it + 3 < nfull; ++it) {
     float lv[16];
-    scores(it, s_cur);
-    read_lse(it, lv);
+    scores(it % 3, s_cur);
+    read_lse(it % 3, lv);
     acc_plain(s_cur, lv);
-    store_tile(it + 2);
-    load_tile(it + 3);
+    store_tile((it + 2) % 3);
+    load_tile(it + 3, Full{});
     __syncthreads();
   }
   for (; it < nit; ++it) step(it, std::integral_constant<bool, false>{});
