@@ -112,7 +112,7 @@ def cpu_baseline(wl, n_layers: int) -> dict:
 def main() -> int:
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="c3_7b_28layer")
     ap.add_argument("--cpu-sample-layers", type=int, default=4)

@@ -54,6 +54,17 @@ __device__ __forceinline__ double inv_freq(int j, int d, double base) {
   return pow(base, (-2.0 * (double)j) / (double)d);
 }
 
+// bf16 element i of a 16-byte piece
+__device__ __forceinline__ uint16_t half16(const uint4 &v, int i) {
+  const uint32_t w = (i >> 1) == 0 ? v.x : (i >> 1) == 1 ? v.y : (i >> 1) == 2 ? v.z : v.w;
+  return (uint16_t)((i & 1) ? (w >> 16) : (w & 0xFFFFu));
+}
+
+__device__ __forceinline__ uint4 shfl_xor4(uint4 v, int m) {
+  return uint4{(uint32_t)__shfl_xor((int)v.x, m), (uint32_t)__shfl_xor((int)v.y, m),
+               (uint32_t)__shfl_xor((int)v.z, m), (uint32_t)__shfl_xor((int)v.w, m)};
+}
+
 // Index f of the first kept entry of the "tight" suffix kept[j] = T - M + j
 // (the newest candidates all kept); the newest evicted candidate is
 // T - M + f - 1 and exactly f kept entries precede it.  Tightness is closed
@@ -333,7 +344,10 @@ __global__ __launch_bounds__(RT) void mrope_rank(RankArgs a) {
 // gather with summary insertion and re-indexing: one wave per output row
 // ---------------------------------------------------------------------------
 
+// 16-byte pieces of a row held by one lane: piece lane + 64 g for g < PG.
+template <int PG>
 __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
+  constexpr int RW = 4;   // rows per wave whose loads are all issued before the first is computed
   const int jj = blockIdx.y;
   const int l = a.layer_id[jj];
   const LayerTable &L = a.tab[l];
@@ -342,9 +356,9 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
   const int dst_buf = inplace ? cur : cur ^ 1;
   const int rows = a.row_start[jj + 1] - a.row_start[jj];
   const int RE = a.row_elems, d = a.head_dim, hd = d / 2;
-  const int npairs = RE / 2, pieces = RE / 8;
+  const int pieces = RE / 8;
   const bool rot = a.reindex == 1 || (a.reindex == 2 && a.flag[0] != 0);
-  if (inplace && !rot) return;
+  if ((inplace && !rot) || pieces > 64 * PG) return;
   const bool has_sum = a.has_sum[jj] != 0;
   const int ins = has_sum ? a.sum_meta[4 * l] : -1;
   const int32_t *kept = a.kept + l * a.kept_lstride;
@@ -352,82 +366,129 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
   uint16_t *Kd = L.k[dst_buf], *Vd = L.v[dst_buf];
   const int32_t *Ps = L.pos[cur], *Rs = L.rpos[cur];
   int32_t *Pd = L.pos[dst_buf], *Rd = L.rpos[dst_buf];
-  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const double invf = inv_freq(lane % hd, d, a.theta);
+  // wave-uniform values are moved to scalar registers (readfirstlane)
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6), lane = threadIdx.x & 63;
+  // Lane f evaluates frequency f % (d/2); the lane holding piece c needs the
+  // 8 frequencies from 8 (c % (d/16)) on, and the other half of each of its
+  // pairs sits in piece c ^ (d/16), held by lane lane ^ (d/16).
+  const int fj = lane % hd;
+  const double invf = inv_freq(fj, d, a.theta);
+  const int pm = d / 16;
+  const int f0 = 8 * (lane % pm);
+  const bool second = (lane & pm) != 0;
   // M-RoPE: the section (0 = t, 1 = h, 2 = w) of this lane's frequency
   const bool three = a.axes == 3;
-  const int fj = lane % hd;
   const int my_axis = fj < a.section[0] ? 0 : fj < a.section[0] + a.section[1] ? 1 : 2;
   const int32_t *Hs = three ? L.rpos_h[cur] : nullptr, *Ws = three ? L.rpos_w[cur] : nullptr;
   int32_t *Hd = three ? L.rpos_h[dst_buf] : nullptr, *Wd = three ? L.rpos_w[dst_buf] : nullptr;
   const int32_t *nc = three ? a.newc + (int64_t)l * 3 * a.newc_lstride : nullptr;
+  __shared__ double2 trig[NT / 64][64];   // (cos, sin) by frequency, one row per wave
 
-  for (int j = blockIdx.x * 4 + wave; j < rows; j += gridDim.x * 4) {
-    // source of output row j
-    const bool is_sum = has_sum && j == ins;
-    const uint16_t *kr, *vr;
-    int p_src, r_src, src_row;
-    if (inplace) {
-      kr = Ks + (int64_t)j * RE;
-      vr = nullptr;
-      p_src = Ps[j];
-      r_src = Rs[j];
-      src_row = j;
-    } else if (is_sum) {
-      kr = a.sum_k + (int64_t)l * RE;
-      vr = a.sum_v + (int64_t)l * RE;
-      p_src = a.sum_meta[4 * l + 1];
-      r_src = a.sum_meta[4 * l + 2];
-      src_row = -1;
-    } else {
-      const int src = min(max(kept[j - (has_sum && j > ins ? 1 : 0)], 0), L.cap - 1);
-      kr = Ks + (int64_t)src * RE;
-      vr = Vs + (int64_t)src * RE;
-      p_src = Ps[src];
-      r_src = Rs[src];
-      src_row = src;
-    }
-    int r_new = rot ? a.rope_offset + j : r_src;
-    int delta = r_new - r_src;
-    int h_old = 0, w_old = 0, h_new = 0, w_new = 0;
-    if (three) {   // no summary rows with M-RoPE: src_row >= 0
-      h_old = Hs[src_row];
-      w_old = Ws[src_row];
-      r_new = rot ? nc[j] : r_src;
-      h_new = rot ? nc[a.newc_lstride + j] : h_old;
-      w_new = rot ? nc[2 * a.newc_lstride + j] : w_old;
-      delta = my_axis == 0 ? r_new - r_src : my_axis == 1 ? h_new - h_old : w_new - w_old;
-    }
-    uint16_t *kd = Kd + (int64_t)j * RE;
-    if (__any(delta != 0)) {   // uniform over the wave (one row)
-      double sn, cs;
-      sincos((double)delta * invf, &sn, &cs);
+  const int stride = gridDim.x * (NT / 64);
+  for (int j0 = blockIdx.x * (NT / 64) + wave; j0 < rows; j0 += stride * RW) {
+    // sources of this wave's rows j0 + u * stride (every value is wave-uniform)
+    const uint16_t *kr[RW], *vr[RW];
+    int src[RW], p_src[RW], r_src[RW];
 #pragma unroll
-      for (int q = 0; q < kMaxPairSlots; ++q) {
-        const int p = lane + 64 * q;
-        if (p >= npairs) break;
-        const int e1 = (p / hd) * d + (p % hd), e2 = e1 + hd;
-        const double x1 = bf16_to_f64(kr[e1]), x2 = bf16_to_f64(kr[e2]);
-        const uint16_t y1 = f64_to_bf16(x1 * cs - x2 * sn);
-        const uint16_t y2 = f64_to_bf16(x2 * cs + x1 * sn);
-        kd[e1] = y1;
-        kd[e2] = y2;
+    for (int u = 0; u < RW; ++u) {
+      const int j = min(j0 + u * stride, rows - 1);
+      if (inplace) {
+        kr[u] = Kd + (int64_t)j * RE;
+        vr[u] = nullptr;
+        src[u] = j;
+        p_src[u] = 0;
+        r_src[u] = __builtin_amdgcn_readfirstlane(Rs[j]);
+      } else if (has_sum && j == ins) {
+        kr[u] = a.sum_k + (int64_t)l * RE;
+        vr[u] = a.sum_v + (int64_t)l * RE;
+        src[u] = -1;
+        p_src[u] = a.sum_meta[4 * l + 1];
+        r_src[u] = a.sum_meta[4 * l + 2];
+      } else {
+        src[u] = __builtin_amdgcn_readfirstlane(
+            min(max(kept[j - (has_sum && j > ins ? 1 : 0)], 0), L.cap - 1));
+        kr[u] = Ks + (int64_t)src[u] * RE;
+        vr[u] = Vs + (int64_t)src[u] * RE;
+        p_src[u] = __builtin_amdgcn_readfirstlane(Ps[src[u]]);
+        r_src[u] = __builtin_amdgcn_readfirstlane(Rs[src[u]]);
       }
-    } else if (!inplace) {
-      for (int c = lane; c < pieces; c += 64)
-        *reinterpret_cast<uint4 *>(kd + 8 * c) = *reinterpret_cast<const uint4 *>(kr + 8 * c);
     }
-    if (!inplace) {
+    uint4 kx[RW][PG], vx[RW][PG];
+#pragma unroll
+    for (int u = 0; u < RW; ++u) {
+#pragma unroll
+      for (int g = 0; g < PG; ++g) {
+        const int c = lane + 64 * g;
+        kx[u][g] = vx[u][g] = uint4{0u, 0u, 0u, 0u};
+        if (c < pieces) {
+          kx[u][g] = *reinterpret_cast<const uint4 *>(kr[u] + 8 * c);
+          if (!inplace) vx[u][g] = *reinterpret_cast<const uint4 *>(vr[u] + 8 * c);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < RW; ++u) {
+      const int j = j0 + u * stride;
+      if (j >= rows) break;
+      int r_new = rot ? a.rope_offset + j : r_src[u];
+      int delta = r_new - r_src[u];
+      int h_old = 0, w_old = 0, h_new = 0, w_new = 0;
+      if (three) {   // no summary rows with M-RoPE: src >= 0
+        h_old = Hs[src[u]];
+        w_old = Ws[src[u]];
+        r_new = rot ? nc[j] : r_src[u];
+        h_new = rot ? nc[a.newc_lstride + j] : h_old;
+        w_new = rot ? nc[2 * a.newc_lstride + j] : w_old;
+        delta = my_axis == 0 ? r_new - r_src[u] : my_axis == 1 ? h_new - h_old : w_new - w_old;
+      }
+      uint4 out[PG];
+#pragma unroll
+      for (int g = 0; g < PG; ++g) out[g] = kx[u][g];
+      if (__any(delta != 0)) {   // uniform over the wave (one row)
+        double sn, cs;
+        sincos((double)delta * invf, &sn, &cs);
+        trig[wave][lane] = double2{cs, sn};
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+#pragma unroll
+        for (int g = 0; g < PG; ++g) {
+          const uint4 px = shfl_xor4(kx[u][g], pm);
+          uint32_t w[4];
+#pragma unroll
+          for (int i = 0; i < 8; i += 2) {
+            uint32_t h2 = 0;
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+              const double2 t = trig[wave][f0 + i + h];
+              const double x = bf16_to_f64(half16(kx[u][g], i + h));
+              const double y = bf16_to_f64(half16(px, i + h));
+              // first half: x cos - y sin; second half: x cos + y sin
+              // (y is the other half of the pair), products rounded apart
+              const double xc = __dmul_rn(x, t.x), ys = __dmul_rn(y, t.y);
+              h2 |= (uint32_t)f64_to_bf16(second ? __dadd_rn(xc, ys) : __dsub_rn(xc, ys)) << (16 * h);
+            }
+            w[i >> 1] = h2;
+          }
+          out[g] = uint4{w[0], w[1], w[2], w[3]};
+        }
+        __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+      }
+      uint16_t *kd = Kd + (int64_t)j * RE;
       uint16_t *vd = Vd + (int64_t)j * RE;
-      for (int c = lane; c < pieces; c += 64)
-        *reinterpret_cast<uint4 *>(vd + 8 * c) = *reinterpret_cast<const uint4 *>(vr + 8 * c);
-      if (lane == 0) Pd[j] = p_src;
-    }
-    if (lane == 0) {
-      Rd[j] = r_new;
-      if (three) {
-        Hd[j] = h_new;
-        Wd[j] = w_new;
+#pragma unroll
+      for (int g = 0; g < PG; ++g) {
+        const int c = lane + 64 * g;
+        if (c < pieces) {
+          *reinterpret_cast<uint4 *>(kd + 8 * c) = out[g];
+          if (!inplace) *reinterpret_cast<uint4 *>(vd + 8 * c) = vx[u][g];
+        }
+      }
+      if (lane == 0) {
+        if (!inplace) Pd[j] = p_src[u];
+        Rd[j] = r_new;
+        if (three) {
+          Hd[j] = h_new;
+          Wd[j] = w_new;
+        }
       }
     }
   }
@@ -458,8 +519,12 @@ hipError_t launch_mrope_rank(const RankArgs &a, hipStream_t s) {
 hipError_t launch_gather_rope(const GatherArgs &a, hipStream_t s) {
   int max_rows = 0;
   for (int j = 0; j < a.n_list; ++j) max_rows = max(max_rows, a.row_start[j + 1] - a.row_start[j]);
-  const int blocks = min((max_rows + 3) / 4, 2048);
-  hipLaunchKernelGGL(gather_rope, dim3(max(blocks, 1), a.n_list), dim3(NT), 0, s, a);
+  // four rows per wave, four waves per workgroup
+  const int blocks = max(1, min((max_rows + 15) / 16, 1024));
+  if (a.row_elems / 8 <= 64)
+    hipLaunchKernelGGL(gather_rope<1>, dim3(blocks, a.n_list), dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL(gather_rope<2>, dim3(blocks, a.n_list), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
