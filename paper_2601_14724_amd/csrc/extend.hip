@@ -65,26 +65,28 @@ __device__ __forceinline__ uint4 shfl_xor4(uint4 v, int m) {
                (uint32_t)__shfl_xor((int)v.z, m), (uint32_t)__shfl_xor((int)v.w, m)};
 }
 
-// Index f of the first kept entry of the "tight" suffix kept[j] = T - M + j
-// (the newest candidates all kept); the newest evicted candidate is
-// T - M + f - 1 and exactly f kept entries precede it.  Tightness is closed
-// upwards, so a binary search finds f.  Requires T > M.
-__device__ int first_tight(const int32_t *kept, int T, int M) {
-  int lo = 0, hi = M;
-  while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (kept[mid] == T - M + mid) hi = mid;
-    else lo = mid + 1;
-  }
-  return lo;
-}
-
-__device__ int lower_bound(const int32_t *a, int n, int x) {
+// The first index in [0, n) where the monotone predicate (false, then true)
+// holds, or n; searched by one whole wave.  Each round the 64 lanes probe 64
+// evenly spaced points of the open interval and a ballot picks the segment,
+// so n entries take about log64(n) dependent loads instead of log2(n).
+// Invariant: the answer lies in [lo, hi], and hi is n or a known true index
+// (probes at or beyond hi count as true).
+template <class Pred>
+__device__ int wave_search(int n, Pred pred) {
+  const int lane = threadIdx.x & 63;
   int lo = 0, hi = n;
   while (lo < hi) {
-    const int mid = (lo + hi) >> 1;
-    if (a[mid] < x) lo = mid + 1;
-    else hi = mid;
+    const int step = (hi - lo + 63) / 64;
+    const int p = lo + (lane + 1) * step - 1;
+    const unsigned long long m = __ballot(p >= hi || pred(p));
+    if (m == 0ull) {
+      lo = hi;
+    } else {
+      const int k = __builtin_ctzll(m);
+      const int pk = lo + (k + 1) * step - 1;
+      lo += k * step;
+      hi = min(hi, pk);
+    }
   }
   return lo;
 }
@@ -93,6 +95,8 @@ __device__ int lower_bound(const int32_t *a, int n, int x) {
 // summary token: per-block fp64 sums of the evicted rows
 // ---------------------------------------------------------------------------
 
+// PG: 16-byte pieces per lane (the row has at most 64 * PG pieces).
+template <int PG>
 __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   const int jj = blockIdx.y;
   const int l = a.layer_id[jj];
@@ -100,7 +104,7 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   const int cur = a.cur[jj];
   const int T = a.len[jj], M = a.budget[jj];
   const int r0 = blockIdx.x * kSummaryRows;
-  if (r0 >= T) return;
+  if (r0 >= T || a.row_elems / 8 > 64 * PG) return;
   const int r1 = min(T, r0 + kSummaryRows);
   const int32_t *kept = a.kept + l * a.kept_lstride;
   const int32_t *rpos = L.rpos[cur];
@@ -111,13 +115,22 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
 
   __shared__ int s_t, s_k0, s_k1;
   __shared__ uint8_t is_kept[kSummaryRows];
-  __shared__ double red[4][2 * 64 * kMaxPairSlots * 2];
+  __shared__ double red[4][2 * 64 * 8 * PG];
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
-  if (tid == 0) {
-    const int f = first_tight(kept, T, M);
-    s_t = rpos[T - M + f - 1];
-    s_k0 = lower_bound(kept, M, r0);
-    s_k1 = lower_bound(kept, M, r1);
+  // Three wave-parallel searches of the kept list, one per wave.  The tight
+  // suffix kept[j] = T - M + j (the newest candidates, all kept) starts at f,
+  // so the newest evicted candidate is T - M + f - 1; tightness holds from f
+  // on (kept is strictly increasing and kept[j] <= T - M + j), which makes it
+  // a monotone predicate.
+  if (wave == 0) {
+    const int f = wave_search(M, [&](int j) { return kept[j] == T - M + j; });
+    if (lane == 0) s_t = rpos[T - M + f - 1];
+  } else if (wave == 1) {
+    const int k0 = wave_search(M, [&](int j) { return kept[j] >= r0; });
+    if (lane == 0) s_k0 = k0;
+  } else if (wave == 2) {
+    const int k1 = wave_search(M, [&](int j) { return kept[j] >= r1; });
+    if (lane == 0) s_k1 = k1;
   }
   for (int i = tid; i < kSummaryRows; i += NT) is_kept[i] = 0;
   __syncthreads();
@@ -125,39 +138,75 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   __syncthreads();
   const int t = s_t;
 
-  const double invf = inv_freq(lane % hd, d, a.theta);
-  double ak[kMaxPairSlots][2], av[kMaxPairSlots][2];
+  // Lane c sums the 16-byte pieces c and c + 64 of the evicted rows' K
+  // (turned to t) and V, in row order; the turn uses the pair partner from
+  // the lane whose piece index differs in bit d/16 and one fp64 sine/cosine
+  // per lane and row (lane f evaluates frequency f % (d/2)), shared through
+  // LDS.  Four rows are loaded before the first is summed.
+  constexpr int RW = 4;
+  const int pieces = RE / 8;
+  const int fj = lane % hd;
+  const double invf = inv_freq(fj, d, a.theta);
+  const int pm = d / 16;
+  const int f0 = 8 * (lane % pm);
+  const bool second = (lane & pm) != 0;
+  __shared__ double2 trig[NT / 64][64];
+  double ak[PG][8], av[PG][8];
 #pragma unroll
-  for (int q = 0; q < kMaxPairSlots; ++q) ak[q][0] = ak[q][1] = av[q][0] = av[q][1] = 0.0;
-  for (int i = r0 + wave; i < r1; i += 4) {
-    if (is_kept[i - r0]) continue;
-    const double ang = (double)(t - rpos[i]) * invf;
-    double sn, cs;
-    sincos(ang, &sn, &cs);
-    const uint16_t *kr = K + (int64_t)i * RE;
-    const uint16_t *vr = V + (int64_t)i * RE;
+  for (int g = 0; g < PG; ++g)
 #pragma unroll
-    for (int q = 0; q < kMaxPairSlots; ++q) {
-      const int p = lane + 64 * q;
-      if (p >= npairs) break;
-      const int e1 = (p / hd) * d + (p % hd), e2 = e1 + hd;
-      const double x1 = bf16_to_f64(kr[e1]), x2 = bf16_to_f64(kr[e2]);
-      ak[q][0] += x1 * cs - x2 * sn;
-      ak[q][1] += x2 * cs + x1 * sn;
-      av[q][0] += bf16_to_f64(vr[e1]);
-      av[q][1] += bf16_to_f64(vr[e2]);
+    for (int i = 0; i < 8; ++i) ak[g][i] = av[g][i] = 0.0;
+  for (int i0 = r0 + wave; i0 < r1; i0 += 4 * RW) {
+    uint4 kx[RW][PG], vx[RW][PG];
+    bool ev[RW];
+#pragma unroll
+    for (int u = 0; u < RW; ++u) {
+      const int i = i0 + 4 * u;
+      ev[u] = i < r1 && !is_kept[i - r0];
+#pragma unroll
+      for (int g = 0; g < PG; ++g) {
+        const int c = lane + 64 * g;
+        kx[u][g] = vx[u][g] = uint4{0u, 0u, 0u, 0u};
+        if (ev[u] && c < pieces) {
+          kx[u][g] = *reinterpret_cast<const uint4 *>(K + (int64_t)i * RE + 8 * c);
+          vx[u][g] = *reinterpret_cast<const uint4 *>(V + (int64_t)i * RE + 8 * c);
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < RW; ++u) {
+      if (!ev[u]) continue;   // uniform over the wave (one row)
+      const int i = i0 + 4 * u;
+      double sn, cs;
+      sincos((double)(t - rpos[i]) * invf, &sn, &cs);
+      trig[wave][lane] = double2{cs, sn};
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+#pragma unroll
+      for (int g = 0; g < PG; ++g) {
+        const uint4 px = shfl_xor4(kx[u][g], pm);
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+          const double2 tr = trig[wave][f0 + e];
+          const double x = bf16_to_f64(half16(kx[u][g], e)), y = bf16_to_f64(half16(px, e));
+          // first half of a pair: x cos - y sin; second half: x cos + y sin
+          ak[g][e] += second ? x * tr.x + y * tr.y : x * tr.x - y * tr.y;
+          av[g][e] += bf16_to_f64(half16(vx[u][g], e));
+        }
+      }
+      __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
     }
   }
   // waves combine in a fixed order: element e of K at [e], of V at [RE + e]
 #pragma unroll
-  for (int q = 0; q < kMaxPairSlots; ++q) {
-    const int p = lane + 64 * q;
-    if (p >= npairs) break;
-    const int e1 = (p / hd) * d + (p % hd), e2 = e1 + hd;
-    red[wave][e1] = ak[q][0];
-    red[wave][e2] = ak[q][1];
-    red[wave][RE + e1] = av[q][0];
-    red[wave][RE + e2] = av[q][1];
+  for (int g = 0; g < PG; ++g) {
+    const int c = lane + 64 * g;
+    if (c < pieces) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        red[wave][8 * c + e] = ak[g][e];
+        red[wave][RE + 8 * c + e] = av[g][e];
+      }
+    }
   }
   __syncthreads();
   double *out = a.part + l * a.part_lstride + (int64_t)blockIdx.x * 2 * RE;
@@ -167,7 +216,8 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
 // Mean over the blocks in block order, rounded to bf16, plus the summary's
 // insert index, stream position and RoPE position.
 __global__ __launch_bounds__(NT) void summary_finalize(SummaryArgs a) {
-  const int jj = blockIdx.x;
+  // grid (element blocks, layers): thread e sums element e over the blocks
+  const int jj = blockIdx.y;
   const int l = a.layer_id[jj];
   const LayerTable &L = a.tab[l];
   const int cur = a.cur[jj];
@@ -176,22 +226,25 @@ __global__ __launch_bounds__(NT) void summary_finalize(SummaryArgs a) {
   const int nb = (T + kSummaryRows - 1) / kSummaryRows;
   const double inv_e = 1.0 / (double)(T - M);
   const double *part = a.part + l * a.part_lstride;
-  for (int e = threadIdx.x; e < 2 * RE; e += NT) {
+  const int e = blockIdx.x * NT + threadIdx.x;
+  if (e < 2 * RE) {
     double s = 0.0;
     for (int b = 0; b < nb; ++b) s += part[(int64_t)b * 2 * RE + e];
     const uint16_t x = f64_to_bf16(s * inv_e);
     if (e < RE) a.sum_k[(int64_t)l * RE + e] = x;
     else a.sum_v[(int64_t)l * RE + e - RE] = x;
   }
-  if (threadIdx.x == 0) {
+  if (blockIdx.x == 0 && threadIdx.x < 64) {
     const int32_t *kept = a.kept + l * a.kept_lstride;
-    const int f = first_tight(kept, T, M);
-    const int newest = T - M + f - 1;
-    int32_t *meta = a.sum_meta + 4 * l;
-    meta[0] = f;                       // kept entries before it
-    meta[1] = L.pos[cur][newest];
-    meta[2] = L.rpos[cur][newest];
-    meta[3] = T - M;                   // tokens folded in
+    const int f = wave_search(M, [&](int j) { return kept[j] == T - M + j; });
+    if (threadIdx.x == 0) {
+      const int newest = T - M + f - 1;
+      int32_t *meta = a.sum_meta + 4 * l;
+      meta[0] = f;                       // kept entries before it
+      meta[1] = L.pos[cur][newest];
+      meta[2] = L.rpos[cur][newest];
+      meta[3] = T - M;                   // tokens folded in
+    }
   }
 }
 
@@ -498,10 +551,13 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
 
 hipError_t launch_summary(const SummaryArgs &a, int max_T, hipStream_t s) {
   const int nb = (max_T + kSummaryRows - 1) / kSummaryRows;
-  hipLaunchKernelGGL(summary_partial, dim3(nb, a.n_list), dim3(NT), 0, s, a);
+  if (a.row_elems / 8 <= 64)
+    hipLaunchKernelGGL(summary_partial<1>, dim3(nb, a.n_list), dim3(NT), 0, s, a);
+  else
+    hipLaunchKernelGGL(summary_partial<2>, dim3(nb, a.n_list), dim3(NT), 0, s, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(summary_finalize, dim3(a.n_list), dim3(NT), 0, s, a);
+  hipLaunchKernelGGL(summary_finalize, dim3((2 * a.row_elems + NT - 1) / NT, a.n_list), dim3(NT), 0, s, a);
   return hipGetLastError();
 }
 
