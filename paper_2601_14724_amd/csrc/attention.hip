@@ -626,7 +626,7 @@ __global__ __launch_bounds__(kNormBlock) void mass_reduce(ColsumArgs a) {
   const int j = blockIdx.y;
   const int layer = a.layer_id[j];
   const int T = a.ncand[j];
-  if (blockIdx.x * kNormBlock >= T) return;   // whole block past this layer's end
+  if ((int)blockIdx.x * kNormBlock >= T) return;   // whole block past this layer's end
   const int i = blockIdx.x * kNormBlock + threadIdx.x;
   double m = 0.0;
   if (i < T) {

@@ -39,7 +39,8 @@ namespace hermes {
 namespace {
 
 constexpr int NT = 256;
-constexpr int kMaxPairSlots = 8;   // Hkv * d / 2 <= 64 * 8 rotate pairs per row
+// Rows of the summary and re-indexing kernels hold at most 1024 elements
+// (Hkv * d <= 1024, checked by the host): at most two 16-byte pieces per lane.
 
 __device__ __forceinline__ double bf16_to_f64(uint16_t b) {
   return (double)__builtin_bit_cast(float, (uint32_t)b << 16);
@@ -111,7 +112,6 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   const uint16_t *K = L.k[cur];
   const uint16_t *V = L.v[cur];
   const int RE = a.row_elems, d = a.head_dim, hd = d / 2;
-  const int npairs = RE / 2;
 
   __shared__ int s_t, s_k0, s_k1;
   __shared__ uint8_t is_kept[kSummaryRows];

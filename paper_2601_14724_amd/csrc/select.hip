@@ -506,7 +506,7 @@ __global__ __launch_bounds__(NT) void score_keys(SelectArgs a) {
   const int tid = threadIdx.x;
   const int l = a.layer_id[blockIdx.y];
   const int T = a.len[l];
-  if (blockIdx.x * MCH >= T) return;   // whole block past the layer's end (uniform)
+  if ((int)blockIdx.x * MCH >= T) return;   // whole block past the layer's end (uniform)
   const LayerTable &L0 = a.tab[l];
   const int C = a.C;
   const int T0 = T - C;
