@@ -228,8 +228,16 @@ __global__ __launch_bounds__(NT) void summary_finalize(SummaryArgs a) {
   const double *part = a.part + l * a.part_lstride;
   const int e = blockIdx.x * NT + threadIdx.x;
   if (e < 2 * RE) {
+    // eight loads in flight, then their sums in block order
     double s = 0.0;
-    for (int b = 0; b < nb; ++b) s += part[(int64_t)b * 2 * RE + e];
+    for (int b0 = 0; b0 < nb; b0 += 8) {
+      double x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) x[u] = b0 + u < nb ? part[(int64_t)(b0 + u) * 2 * RE + e] : 0.0;
+#pragma unroll
+      for (int u = 0; u < 8; ++u)
+        if (b0 + u < nb) s += x[u];
+    }
     const uint16_t x = f64_to_bf16(s * inv_e);
     if (e < RE) a.sum_k[(int64_t)l * RE + e] = x;
     else a.sum_v[(int64_t)l * RE + e - RE] = x;
@@ -442,6 +450,7 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
     // sources of this wave's rows j0 + u * stride (every value is wave-uniform)
     const uint16_t *kr[RW], *vr[RW];
     int src[RW], p_src[RW], r_src[RW];
+    int h_old[RW], w_old[RW], c_new[RW][3];   // M-RoPE coordinates before / after
 #pragma unroll
     for (int u = 0; u < RW; ++u) {
       const int j = min(j0 + u * stride, rows - 1);
@@ -465,6 +474,14 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
         p_src[u] = __builtin_amdgcn_readfirstlane(Ps[src[u]]);
         r_src[u] = __builtin_amdgcn_readfirstlane(Rs[src[u]]);
       }
+      h_old[u] = w_old[u] = c_new[u][0] = c_new[u][1] = c_new[u][2] = 0;
+      if (three) {   // no summary rows with M-RoPE: src >= 0
+        h_old[u] = __builtin_amdgcn_readfirstlane(Hs[src[u]]);
+        w_old[u] = __builtin_amdgcn_readfirstlane(Ws[src[u]]);
+#pragma unroll
+        for (int x = 0; x < 3; ++x)
+          c_new[u][x] = __builtin_amdgcn_readfirstlane(nc[x * a.newc_lstride + j]);
+      }
     }
     uint4 kx[RW][PG], vx[RW][PG];
 #pragma unroll
@@ -485,14 +502,12 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
       if (j >= rows) break;
       int r_new = rot ? a.rope_offset + j : r_src[u];
       int delta = r_new - r_src[u];
-      int h_old = 0, w_old = 0, h_new = 0, w_new = 0;
-      if (three) {   // no summary rows with M-RoPE: src >= 0
-        h_old = Hs[src[u]];
-        w_old = Ws[src[u]];
-        r_new = rot ? nc[j] : r_src[u];
-        h_new = rot ? nc[a.newc_lstride + j] : h_old;
-        w_new = rot ? nc[2 * a.newc_lstride + j] : w_old;
-        delta = my_axis == 0 ? r_new - r_src[u] : my_axis == 1 ? h_new - h_old : w_new - w_old;
+      int h_new = 0, w_new = 0;
+      if (three) {
+        r_new = rot ? c_new[u][0] : r_src[u];
+        h_new = rot ? c_new[u][1] : h_old[u];
+        w_new = rot ? c_new[u][2] : w_old[u];
+        delta = my_axis == 0 ? r_new - r_src[u] : my_axis == 1 ? h_new - h_old[u] : w_new - w_old[u];
       }
       uint4 out[PG];
 #pragma unroll
