@@ -26,7 +26,8 @@ typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short s4 __attribute__((ext_vector_type(4)));
 
-constexpr int BM = kAttnRowsPerBlock;    // packed rows per workgroup (4 waves x 32)
+constexpr int AT = 512;                  // attention workgroup: 8 waves, two per SIMD
+constexpr int BM = kAttnRowsPerBlock;    // packed rows per workgroup (8 waves x 32)
 constexpr int BN = 64;                   // keys per tile
 constexpr int BK = kColsumKeysPerBlock;  // candidates per sweep workgroup (4 waves x 64)
 constexpr int BQS = 32;                  // packed rows per sweep tile
@@ -74,7 +75,7 @@ __device__ __forceinline__ int xcd_remap(int i, int n) {
 // WRITE_O: store O (chunk and query passes); without it only the row LSE is
 // written (guidance-prompt passes).
 template <int D, bool SPLIT, bool WRITE_O>
-__global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
+__global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   // Consecutive ids: the query tiles of one (layer, KV head[, key slice]),
   // which stream the same K/V.
@@ -132,7 +133,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN][D + VPAD];
 
   constexpr int CH = D / 8;                 // 16-byte chunks per key row and head
-  constexpr int NLD = BN * CH / 256;        // chunks per thread per tensor
+  constexpr int NLD = BN * CH / AT;         // chunks per thread per tensor
   const int64_t row_stride = (int64_t)Hkv * D;
   uint4 kreg[NLD], vreg[NLD];
   // Tiles [0, n_pure) lie wholly in the cache and below every row's causal
@@ -143,7 +144,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   uint32_t cofs[NLD];
 #pragma unroll
   for (int u = 0; u < NLD; ++u) {
-    const int e = tid + u * 256;
+    const int e = tid + u * AT;
     cofs[u] = (uint32_t)(((e / CH) * row_stride + kv * D + (e % CH) * 8) * sizeof(uint16_t));
   }
   auto load_pure = [&](int k0) {
@@ -158,7 +159,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   auto load_any = [&](int k0) {
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      const int e = tid + u * 256;
+      const int e = tid + u * AT;
       const int kr = e / CH, ch = e % CH;
       const int i = k0 + kr;
       uint4 k4 = {0u, 0u, 0u, 0u}, v4 = {0u, 0u, 0u, 0u};
@@ -174,7 +175,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd(AttnArgs a, int nqt) {
   auto store_tile = [&](int b) {
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      const int e = tid + u * 256;
+      const int e = tid + u * AT;
       const int kr = e / CH, ch = e % CH;
       *reinterpret_cast<uint4 *>(&Ks[b][kr][ch * 8]) = kreg[u];
       *reinterpret_cast<uint4 *>(&Vs[b][kr][ch * 8]) = vreg[u];
@@ -657,11 +658,11 @@ hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStre
   dim3 grid(nqt * a.Hkv * n_list);
   const bool wo = a.out != nullptr;
   if (head_dim == 64) {
-    if (wo) hipLaunchKernelGGL((attn_fwd<64, false, true>), grid, dim3(256), 0, s, a, nqt);
-    else hipLaunchKernelGGL((attn_fwd<64, false, false>), grid, dim3(256), 0, s, a, nqt);
+    if (wo) hipLaunchKernelGGL((attn_fwd<64, false, true>), grid, dim3(AT), 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<64, false, false>), grid, dim3(AT), 0, s, a, nqt);
   } else {
-    if (wo) hipLaunchKernelGGL((attn_fwd<128, false, true>), grid, dim3(256), 0, s, a, nqt);
-    else hipLaunchKernelGGL((attn_fwd<128, false, false>), grid, dim3(256), 0, s, a, nqt);
+    if (wo) hipLaunchKernelGGL((attn_fwd<128, false, true>), grid, dim3(AT), 0, s, a, nqt);
+    else hipLaunchKernelGGL((attn_fwd<128, false, false>), grid, dim3(AT), 0, s, a, nqt);
   }
   return hipGetLastError();
 }
@@ -672,12 +673,12 @@ hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, h
   dim3 grid(nqt * a.nsplit * a.Hkv * n_list);
   dim3 cgrid((P * (head_dim / 8) + 255) / 256, a.Hkv, n_list);
   if (head_dim == 64) {
-    hipLaunchKernelGGL((attn_fwd<64, true, true>), grid, dim3(256), 0, s, a, nqt);
+    hipLaunchKernelGGL((attn_fwd<64, true, true>), grid, dim3(AT), 0, s, a, nqt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(attn_combine<64>, cgrid, dim3(256), 0, s, a);
   } else {
-    hipLaunchKernelGGL((attn_fwd<128, true, true>), grid, dim3(256), 0, s, a, nqt);
+    hipLaunchKernelGGL((attn_fwd<128, true, true>), grid, dim3(AT), 0, s, a, nqt);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     hipLaunchKernelGGL(attn_combine<128>, cgrid, dim3(256), 0, s, a);

@@ -131,15 +131,15 @@ Layout layout_of(const hermes_config *c) {
 }
 
 // Key slices for a pass of n_rows rows over caches of at most max_T0 tokens:
-// as many as keep all workgroups in one round of the GPU's slots (two
-// attention workgroups on each of 256 CUs), each slice at least 8 key tiles;
+// as many as keep all workgroups in one round of the GPU's slots (one
+// attention workgroup on each of 256 CUs), each slice at least 8 key tiles;
 // 1 means the plain kernel.  A second round would repeat every workgroup's
 // fixed cost (query load, partial-state write) for no gain in parallelism.
 int split_count(int n_rows, int G, int Hkv, int n_list, int max_T0) {
   if (n_rows > kSplitMaxTokens) return 1;
   const int nqt = (n_rows * G + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
   const int base = nqt * Hkv * n_list;
-  const int want = 512 / base;
+  const int want = 256 / base;
   const int tiles = (max_T0 + n_rows + 63) / 64;
   int s = want < kMaxSplits ? want : kMaxSplits;
   if (s > tiles / 8) s = tiles / 8;

@@ -212,7 +212,7 @@ hipError_t launch_gather_rope(const GatherArgs &a, hipStream_t s);
 hipError_t launch_mrope_rank(const RankArgs &a, hipStream_t s);
 
 // Geometry shared by host sizing and kernels.
-constexpr int kAttnRowsPerBlock = 128;   // packed (row, head) pairs per workgroup
+constexpr int kAttnRowsPerBlock = 256;   // packed (row, head) pairs per attention workgroup
 constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the sweep
 constexpr int kSummaryRows = 128;        // candidates per workgroup of the summary sums
 constexpr int kSplitMaxTokens = 64;      // passes of at most this many rows use split keys
