@@ -116,7 +116,7 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   __shared__ int s_t, s_k0, s_k1;
   __shared__ uint8_t is_kept[kSummaryRows];
   __shared__ double red[4][2 * 64 * 8 * PG];
-  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
   // Three wave-parallel searches of the kept list, one per wave.  The tight
   // suffix kept[j] = T - M + j (the newest candidates, all kept) starts at f,
   // so the newest evicted candidate is T - M + f - 1; tightness holds from f
