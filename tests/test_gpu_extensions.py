@@ -108,7 +108,9 @@ def _check_step(wl, classes, ext, kv, ref, what):
     return compact, reidx
 
 
-@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128)])
+# (32, 8, 128): 1024-element rows, two 16-byte pieces per lane in the
+# summary and re-indexing kernels
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128), (32, 8, 128)])
 @pytest.mark.parametrize("reindex", [he.REINDEX_NONE, he.REINDEX_EAGER])
 def test_summary_tokens(shape, reindex):
     Hq, Hkv, d = shape
@@ -315,7 +317,7 @@ def _grid(n, H, W, offset, t_step):
     return np.stack([offset + f * t_step, offset + r // W, offset + r % W], 1).astype(np.int64)
 
 
-@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128)])
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128), (32, 8, 128)])
 @pytest.mark.parametrize("mode", ["eager", "lazy_fires", "lazy_waits"])
 def test_mrope_reindex(shape, mode):
     """5 cached frames of 14 x 14 tokens (t step 2, text prefix 3) + 1 new
