@@ -109,6 +109,10 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   // This lane's query row (column n of the S^T tile).
   const int prow = p0 + wave * 32 + l32;
   const bool row_ok = prow < P;
+  // A wave whose 32 rows all lie past P (in the last query tile of a head
+  // group) still loads and stores its share of every tile and meets every
+  // barrier, but issues no MFMAs.
+  const bool wave_rows = __builtin_amdgcn_readfirstlane(p0 + wave * 32 < P ? 1 : 0) != 0;
   const int r = row_ok ? prow / G : 0;
   const int h = kv * G + (row_ok ? prow - r * G : 0);
   const int vis = row_ok ? T0 + r : -1;     // last candidate this row sees
@@ -305,13 +309,18 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
       store_tile(t & 1);
       __syncthreads();
       load_pure((t + 1) * BN);
-      compute(t, NoMask{});
+      if (wave_rows) compute(t, NoMask{});
     }
     for (; t < ntiles; ++t) {
       store_tile(t & 1);
       __syncthreads();
       if (t + 1 < ntiles) load_any((t + 1) * BN);
-      if ((t + 1) * BN - 1 > vis_min) compute(t, Mask{}); else compute(t, NoMask{});
+      if (!wave_rows) {
+      } else if ((t + 1) * BN - 1 > vis_min) {
+        compute(t, Mask{});
+      } else {
+        compute(t, NoMask{});
+      }
     }
   } else {
     // this workgroup's slice [t_begin, t_end) of the key tiles
@@ -327,13 +336,18 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
       store_tile(t & 1);
       __syncthreads();
       load_pure((t + 1) * BN);
-      compute(t, NoMask{});
+      if (wave_rows) compute(t, NoMask{});
     }
     for (; t < t_end; ++t) {
       store_tile(t & 1);
       __syncthreads();
       if (t + 1 < t_end) load_any((t + 1) * BN);
-      if ((t + 1) * BN - 1 > vis_min) compute(t, Mask{}); else compute(t, NoMask{});
+      if (!wave_rows) {
+      } else if ((t + 1) * BN - 1 > vis_min) {
+        compute(t, Mask{});
+      } else {
+        compute(t, NoMask{});
+      }
     }
   }
 
@@ -458,10 +472,11 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   const float *lse_l = a.lse + layer * a.lse_lstride;
   const float c = a.scale_log2;
 
-  // Three-deep ring of 32-row query tiles: tile it is read by the MFMAs
-  // while tile it+2 is stored and tile it+3 loaded.
-  __shared__ __attribute__((aligned(16))) uint16_t Qs[3][BQS][D + KPAD];
-  __shared__ __attribute__((aligned(16))) float Ls[3][BQS];
+  // Ring of 32-row query tiles (four slots, so the slot index is a mask):
+  // tile it is read by the MFMAs while tile it+2 is stored and tile it+3
+  // loaded.
+  __shared__ __attribute__((aligned(16))) uint16_t Qs[4][BQS][D + KPAD];
+  __shared__ __attribute__((aligned(16))) float Ls[4][BQS];
 
   constexpr int CH = D / 8;
   constexpr int NLD = BQS * CH / 256;
@@ -588,11 +603,11 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   f32x16 s_cur[2];
   auto step = [&](int it, auto masked) {
     float lv[16];
-    scores(it % 3, s_cur);
-    read_lse(it % 3, lv);
+    scores(it & 3, s_cur);
+    read_lse(it & 3, lv);
     if constexpr (decltype(masked)::value) acc_masked(it, s_cur, lv); else acc_plain(s_cur, lv);
     if (it + 2 < nit) {
-      store_tile((it + 2) % 3);
+      store_tile((it + 2) & 3);
       if (it + 3 < nit) load_tile(it + 3, Edge{});
     }
     __syncthreads();
@@ -602,10 +617,10 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   // steady state: no branches inside the body
   for (; it + 3 < nfull; ++it) {
     float lv[16];
-    scores(it % 3, s_cur);
-    read_lse(it % 3, lv);
+    scores(it & 3, s_cur);
+    read_lse(it & 3, lv);
     acc_plain(s_cur, lv);
-    store_tile((it + 2) % 3);
+    store_tile((it + 2) & 3);
     load_tile(it + 3, Full{});
     __syncthreads();
   }
