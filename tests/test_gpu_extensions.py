@@ -63,7 +63,8 @@ def _cmp_layer(l, kv, exp: he.ExtLayerCache, what):
             assert worst <= 1.0 and diff.mean() <= 1e-4, f"{what} layer {l}: {name} differs"
 
 
-def _run(wl, classes, ext: he.ExtConfig, caches, chunks, prompts=None, **kw):
+def _run(wl, classes, ext: he.ExtConfig, caches, chunks, prompts=None, prompts_stacked=False,
+         **kw):
     kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, layer_class=classes,
                               summary_mode=int(ext.summary), reindex_mode=ext.reindex_mode,
                               rope_offset=ext.rope_offset, rope_limit=ext.rope_limit,
@@ -71,7 +72,11 @@ def _run(wl, classes, ext: he.ExtConfig, caches, chunks, prompts=None, **kw):
                               scoring_mode=ext.scoring_mode, **kw)
     t = streaming.chunk_tensors(_stack(chunks), "cuda")
     kv.append(t["q"], t["k"], t["v"], t["pos"])
-    if prompts is not None:
+    if prompts is not None and prompts_stacked:   # one pass over every layer
+        pt = {k2: streaming.bf16_tensor(np.stack([p[k2] for p in prompts]), "cuda")
+              for k2 in ("q", "k", "v")}
+        kv.guidance(pt["q"], pt["k"], pt["v"])
+    elif prompts is not None:
         for l, p in enumerate(prompts):
             if p is None:
                 continue
@@ -238,6 +243,41 @@ def test_guidance_prompt_scoring():
             assert srel <= 1e-3, f"layer {l}: smoothed key rel {srel}"
         idx = kv.kept_dbg[l].cpu().numpy().astype(np.int64)
         check_kept(idx, ref["smoothed"][l], wl.budgets[l], f"guidance layer {l}")
+    kv.close()
+
+
+def test_guidance_prompt_all_layers_one_pass():
+    """A 64-row prompt for all 28 layers of the 7B head shape in one call:
+    the row pass fills one round of workgroups, so it runs unsliced (the
+    row-LSE-only attention kernel); W, smoothed keys and kept sets against
+    the oracle."""
+    L = 28
+    classes = [S] * 3 + [M] * 17 + [D] * 8
+    wl = _wl("ext_guide_all", 55, L, 28, 4, 128, 256, 64, tuple(200 + 3 * l for l in range(L)))
+    caches = [wk.gen_cache(wl, l) for l in range(L)]
+    chunks = [wk.gen_chunk(wl, 0, l) for l in range(L)]
+    prompts = [wk.gen_prompt(wl, l, 64, wk.PROMPT_HYBRID if classes[l] == M else wk.PROMPT_GLOBAL)
+               for l in range(L)]
+    ext = he.ExtConfig(scoring_mode=he.SCORE_GUIDANCE)
+    say("guidance-prompt scoring, all layers in one pass")
+    kv, w = _run(wl, classes, ext, caches, chunks, prompts=prompts, prompts_stacked=True)
+    cfg = orc.OracleConfig(budgets=list(wl.budgets), classes=classes)
+    pr = [None if classes[l] == S else {"q": f64(p["q"]), "k": f64(p["k"]), "v": f64(p["v"])}
+          for l, p in enumerate(prompts)]
+    ref = he.stream_step_ext(_ext_caches(caches), _ext_chunks(chunks), cfg, ext, prompts=pr)
+    worst = 0.0
+    for l in range(L):
+        T = len(ref["appended"][l].pos)
+        if classes[l] != S:
+            rel = float(np.max(np.abs(w[l][:T] - ref["w"][l]) / ref["w"][l]))
+            worst = max(worst, rel)
+            assert rel <= 1e-3, f"layer {l}: W rel {rel}"
+            sg = kv.s_dbg[l][:T].cpu().numpy().astype(np.float64)
+            srel = float(np.max(np.abs(sg - ref["smoothed"][l]) / ref["smoothed"][l]))
+            assert srel <= 1e-3, f"layer {l}: smoothed key rel {srel}"
+        idx = kv.kept_dbg[l].cpu().numpy().astype(np.int64)
+        check_kept(idx, ref["smoothed"][l], wl.budgets[l], f"guidance layer {l}")
+    say(f"worst W rel {worst:.2e}")
     kv.close()
 
 
