@@ -125,7 +125,7 @@ def main() -> int:
                     help="also run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
-        log("this build runs on one GPU only; --gpus must be 1")
+        log("the streaming step runs on one GPU and is not sharded across GPUs; --gpus must be 1")
         return 2
 
     import torch
