@@ -510,11 +510,9 @@ static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void
   };
 
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const int G = ctx->Hq / ctx->Hkv;
   const int64_t q_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_new * ctx->Hq * ctx->D : 0;
   const int64_t kv_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_new * ctx->Hkv * ctx->D : 0;
   const float scale_log2 = (float)(ctx->sm_scale * kLog2e);
-  (void)G;
 
   AppendArgs ap;
   std::memset(&ap, 0, sizeof(ap));
