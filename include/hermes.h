@@ -340,6 +340,25 @@ int hermes_select_topk(const float *keys, int32_t n, int32_t k, int32_t *out_idx
                        void *stream);
 
 /*
+ * Precondition checks on the device, for callers that want the inputs the
+ * fast path trusts verified: while enabled, hermes_append_chunk (all forms)
+ * first checks that q, k and v hold only finite bf16 values, that pos is
+ * strictly increasing and that pos[0] is greater than the last cached
+ * position of every appended layer (stream positions only grow: the
+ * cross-layer smoothing join and the recency term of Sec. 3.1 / 3.2 rely on
+ * sorted positions); hermes_query_attend and hermes_guidance_score check
+ * that q, k and v are finite.  The check runs on the call's stream and the
+ * call waits for it (one stream synchronisation), so a violation returns
+ * HERMES_EINVAL before anything else is launched: device data and host
+ * lengths are untouched.  Off by default; the environment variable
+ * HERMES_CHECK=1 at hermes_kv_init turns it on for that context.  Uses a
+ * word of the context's workspace; not for use under graph capture.
+ * Errors: EINVAL (null context), EHIP from the check's own launches (the
+ * context is then poisoned).
+ */
+int hermes_check_enable(hermes_ctx *ctx, int on);
+
+/*
  * Kernel timing with HIP events recorded on the launch stream around every
  * launch of one kernel class while enabled.  Kernel ids: 0 append copy,
  * 1 chunk attention, 2 attention-mass sweep, 3 score+select, 4 gather (and

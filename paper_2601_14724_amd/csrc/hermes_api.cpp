@@ -4,6 +4,7 @@
 // leaves device data and host lengths untouched.
 #include <cmath>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <new>
 #include <utility>
@@ -189,6 +190,7 @@ struct hermes_ctx {
   char *ws = nullptr;
   LayerTable *d_tab = nullptr;
   bool prof = false;
+  bool check = false;   // device-side precondition checks before each call's launches
   std::vector<EventPair> used[HERMES_K_COUNT];
   std::vector<EventPair> pool;
 
@@ -231,6 +233,41 @@ struct hermes_ctx {
     return HERMES_OK;
   }
 };
+
+// Device-side precondition checks of one call (when enabled): q, k, v of
+// nq / nkv bf16 elements finite, and, with pos, the chunk positions strictly
+// increasing and after the last cached position of every listed layer.  Waits
+// for the verdict, so a failing call has launched nothing else: EINVAL.
+static int run_checks(hermes_ctx *ctx, const std::vector<int> &list, const void *q, const void *k,
+                      const void *v, int64_t nq, int64_t nkv, const int32_t *pos, int n_new,
+                      hipStream_t s) {
+  if (!ctx->check) return HERMES_OK;
+  CheckArgs ca;
+  std::memset(&ca, 0, sizeof(ca));
+  ca.tab = ctx->d_tab;
+  ca.q = static_cast<const uint16_t *>(q);
+  ca.k = static_cast<const uint16_t *>(k);
+  ca.v = static_cast<const uint16_t *>(v);
+  ca.nq = nq;
+  ca.nkv = nkv;
+  ca.pos = pos;
+  ca.n_new = n_new;
+  ca.n_list = pos != nullptr ? (int)list.size() : 0;
+  for (size_t j = 0; j < list.size(); ++j) {
+    ca.layer_id[j] = (int8_t)list[j];
+    ca.cur[j] = ctx->cur[list[j]];
+    ca.len[j] = ctx->len[list[j]];
+  }
+  ca.flag = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.flag) + 2;   // [0] is the re-indexing decision
+  int32_t verdict = 0;
+  if (hipMemsetAsync(ca.flag, 0, sizeof(int32_t), s) != hipSuccess || launch_check(ca, s) != hipSuccess ||
+      hipMemcpyAsync(&verdict, ca.flag, sizeof(int32_t), hipMemcpyDeviceToHost, s) != hipSuccess ||
+      hipStreamSynchronize(s) != hipSuccess) {
+    ctx->poisoned = true;
+    return HERMES_EHIP;
+  }
+  return verdict == 0 ? HERMES_OK : HERMES_EINVAL;
+}
 
 extern "C" {
 
@@ -355,6 +392,10 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
   c->lay = lay;
   c->ws = static_cast<char *>(workspace);
   c->d_tab = reinterpret_cast<LayerTable *>(c->ws + lay.tab);
+  {
+    const char *env = std::getenv("HERMES_CHECK");
+    c->check = env != nullptr && env[0] == '1';
+  }
 
   std::vector<LayerTable> tab(L);
   for (int l = 0; l < L; ++l) {
@@ -496,6 +537,12 @@ static int append_impl(hermes_ctx *ctx, int32_t layer, const void *q, const void
   if (ctx->n_appended > 0 && n_new != ctx->step_n_new) return HERMES_ESTATE;
   for (int l : list)
     if ((int64_t)ctx->len[l] + n_new > ctx->bufs[l].cap) return HERMES_ECAPACITY;
+  {
+    const int64_t rows = (int64_t)list.size() * n_new;
+    const int rc = run_checks(ctx, list, q, k, v, rows * ctx->Hq * ctx->D, rows * ctx->Hkv * ctx->D, pos,
+                              n_new, static_cast<hipStream_t>(stream));
+    if (rc != HERMES_OK) return rc;
+  }
 
   // Which layers' scores the coming compression needs (Sec. 3.1/3.2): a
   // non-shallow layer that evicts, or whose shallower neighbour evicts and
@@ -638,6 +685,12 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
   for (int l : list)
     if (!ctx->appended[l]) return HERMES_ESTATE;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  {
+    const int64_t rows = (int64_t)list.size() * n_rows;
+    const int rc = run_checks(ctx, list, q, k, v, rows * ctx->Hq * ctx->D, rows * ctx->Hkv * ctx->D, nullptr,
+                              n_rows, s);
+    if (rc != HERMES_OK) return rc;
+  }
   const int64_t q_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_rows * ctx->Hq * ctx->D : 0;
   const int64_t kv_ls = (layer == HERMES_ALL_LAYERS) ? (int64_t)n_rows * ctx->Hkv * ctx->D : 0;
   const float scale_log2 = (float)(ctx->sm_scale * kLog2e);
@@ -905,6 +958,12 @@ int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   if (n_q < 1 || n_q > ctx->max_chunk) return HERMES_EINVAL;
   if (ctx->n_appended != 0) return HERMES_ESTATE;
   hipStream_t s = static_cast<hipStream_t>(stream);
+  {
+    const int64_t rows = (int64_t)(layer == HERMES_ALL_LAYERS ? L : 1) * n_q;
+    const int rc = run_checks(ctx, std::vector<int>(), q, k, v, rows * ctx->Hq * ctx->D,
+                              rows * ctx->Hkv * ctx->D, nullptr, n_q, s);
+    if (rc != HERMES_OK) return rc;
+  }
   AttnArgs at;
   std::memset(&at, 0, sizeof(at));
   at.tab = ctx->d_tab;
@@ -945,6 +1004,12 @@ int hermes_select_topk(const float *keys, int32_t n, int32_t k, int32_t *out_idx
   return launch_topk(keys, n, k, out_idx, static_cast<hipStream_t>(stream)) == hipSuccess
              ? HERMES_OK
              : HERMES_EHIP;
+}
+
+int hermes_check_enable(hermes_ctx *ctx, int on) {
+  if (ctx == nullptr) return HERMES_EINVAL;
+  ctx->check = on != 0;
+  return HERMES_OK;
 }
 
 int hermes_profile_enable(hermes_ctx *ctx, int on) {

@@ -203,6 +203,24 @@ hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, h
 hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_dim,
                          hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
+// Precondition checks (device side): q, k, v bf16 with nq / nkv elements
+// (multiples of 8, 16-byte aligned), the chunk positions pos[0..n_new) (or
+// null) against the last cached position of each listed layer; violations
+// are ORed into *flag.
+struct CheckArgs {
+  const LayerTable *tab;
+  const uint16_t *q, *k, *v;
+  int64_t nq, nkv;
+  const int32_t *pos;
+  int32_t n_new;
+  int32_t n_list;
+  int32_t len[kMaxLayers];
+  int8_t layer_id[kMaxLayers];
+  int8_t cur[kMaxLayers];
+  int32_t *flag;
+};
+
+hipError_t launch_check(const CheckArgs &a, hipStream_t s);
 hipError_t launch_gather(const GatherArgs &a, hipStream_t s);
 hipError_t launch_append(const AppendArgs &a, hipStream_t s);
 hipError_t launch_topk(const float *keys, int n, int k, int32_t *out, hipStream_t s);

@@ -34,7 +34,8 @@ EXPORTED = ("hermes_workspace_bytes", "hermes_kv_init", "hermes_append_chunk",
             "hermes_append_chunk_mrope", "hermes_query_attend", "hermes_kv_rewind",
             "hermes_kv_view", "hermes_kv_view_rope", "hermes_kv_view_mrope",
             "hermes_budget_from_weights", "hermes_kv_destroy", "hermes_strerror",
-            "hermes_select_topk", "hermes_profile_enable", "hermes_profile_read")
+            "hermes_select_topk", "hermes_profile_enable", "hermes_profile_read",
+            "hermes_check_enable")
 
 
 class HermesConfig(ctypes.Structure):
@@ -100,6 +101,8 @@ lib.hermes_strerror.restype = ctypes.c_char_p
 lib.hermes_strerror.argtypes = [ctypes.c_int]
 lib.hermes_select_topk.restype = ctypes.c_int
 lib.hermes_select_topk.argtypes = [_vp, _i32, _i32, _vp, _vp]
+lib.hermes_check_enable.restype = ctypes.c_int
+lib.hermes_check_enable.argtypes = [_vp, ctypes.c_int]
 lib.hermes_profile_enable.restype = ctypes.c_int
 lib.hermes_profile_enable.argtypes = [_vp, ctypes.c_int]
 lib.hermes_profile_read.restype = ctypes.c_int
@@ -367,6 +370,10 @@ class HermesKV:
                             self.rpos_w[layer][p][:n]])
 
     # -------------------------------------------------------------- profiling
+    def check_preconditions(self, on: bool = True) -> None:
+        """Device-side checks of positions and finiteness before each call."""
+        check(lib.hermes_check_enable(self.ctx, int(on)), "hermes_check_enable")
+
     def profile(self, on: bool = True) -> None:
         check(lib.hermes_profile_enable(self.ctx, int(on)), "hermes_profile_enable")
 

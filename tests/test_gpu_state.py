@@ -90,3 +90,62 @@ def test_profiling_counts_launches():
     ms, n = kv.profile_read(H.K_ATTN)
     assert n == 0 and ms == 0
     kv.close()
+
+
+def test_precondition_checks_reject_before_any_launch(monkeypatch):
+    """With device-side checks on, a chunk whose positions are not strictly
+    increasing or not after the cache, or whose inputs are not finite, is
+    rejected with EINVAL and changes nothing; valid inputs give bitwise the
+    same results as an unchecked context."""
+    wl, kv, t = _setup()
+    _, ref, _ = _setup()
+    kv.check_preconditions(True)
+    bad_order = t["pos"].clone()
+    bad_order[3] = bad_order[2]
+    early = t["pos"] - 1                       # first position equals the last cached one
+    q_nan = t["q"].clone()
+    q_nan.view(-1)[5] = float("nan")
+    v_inf = t["v"].clone()
+    v_inf.view(-1)[-1] = float("inf")
+    for q, k, v, pos in ((t["q"], t["k"], t["v"], bad_order), (t["q"], t["k"], t["v"], early),
+                         (q_nan, t["k"], t["v"], t["pos"]), (t["q"], t["k"], v_inf, t["pos"])):
+        with pytest.raises(H.HermesError) as e:
+            kv.append(q, k, v, pos)
+        assert e.value.code == H.EINVAL
+        assert [kv.length(l) for l in range(3)] == [20, 20, 20]
+    one = {k: t[k][1].contiguous() for k in ("q", "k", "v")}
+    bad_one = one["q"].clone()
+    bad_one.view(-1)[0] = float("-inf")
+    with pytest.raises(H.HermesError) as e:   # one layer; earlier ones stay appendable
+        kv.append(bad_one, one["k"], one["v"], t["pos"], layer=1)
+    assert e.value.code == H.EINVAL
+    out = kv.append(t["q"], t["k"], t["v"], t["pos"])
+    out_ref = ref.append(t["q"], t["k"], t["v"], t["pos"])
+    kv.compress()
+    ref.compress()
+    torch.cuda.synchronize()
+    assert torch.equal(out.view(torch.int16), out_ref.view(torch.int16))
+    for l in range(3):
+        a, b = kv.view(l), ref.view(l)
+        assert torch.equal(a[2], b[2])
+        assert torch.equal(a[0].view(torch.int16), b[0].view(torch.int16))
+    with pytest.raises(H.HermesError) as e:   # query inputs are checked for finiteness too
+        kv.query(q_nan, t["k"], t["v"])
+    assert e.value.code == H.EINVAL
+    qo = kv.query(t["q"], t["k"], t["v"])
+    qo_ref = ref.query(t["q"], t["k"], t["v"])
+    torch.cuda.synchronize()
+    assert torch.equal(qo.view(torch.int16), qo_ref.view(torch.int16))
+    kv.close()
+    ref.close()
+    # HERMES_CHECK=1 turns the checks on for contexts created while it is set
+    monkeypatch.setenv("HERMES_CHECK", "1")
+    _, envkv, _ = _setup()
+    with pytest.raises(H.HermesError) as e:
+        envkv.append(t["q"], t["k"], t["v"], bad_order)
+    assert e.value.code == H.EINVAL
+    envkv.check_preconditions(False)          # and the toggle turns them off again: a chunk
+    envkv.append(t["q"], t["k"], t["v"], early)   # overlapping the cache's last position passes
+    torch.cuda.synchronize()
+    assert [envkv.length(l) for l in range(3)] == [28, 28, 28]
+    envkv.close()
