@@ -121,6 +121,8 @@ def main() -> int:
                     help="skip the summary-token / re-indexing / guidance-prompt timings")
     ap.add_argument("--no-c4", action="store_true",
                     help="skip the 64-chunk stream from an empty cache")
+    ap.add_argument("--no-c5", action="store_true",
+                    help="skip the long-cache configuration (32768 + 3136 tokens, 64-token query)")
     ap.add_argument("--calib-copy-mib", type=int, default=0,
                     help="also run one plain device copy of this many MiB (counter calibration)")
     args = ap.parse_args()
@@ -238,6 +240,10 @@ def main() -> int:
     if not args.no_c4 and args.workload == "c3_7b_28layer":
         log("[bench] 64-chunk stream from an empty cache (7B shape, budget 6144)")
         c4 = c4_bench()
+    c5 = None
+    if not args.no_c5 and args.workload == "c3_7b_28layer":
+        log("[bench] long cache: 32768 + 3136 tokens per layer, then a 64-token query")
+        c5 = c5_bench(min(args.steps, 10), min(args.warmup, 3))
     ext = None
     if not args.no_extensions:
         log("[bench] adjacent rows: summary tokens + eager re-indexing, guidance prompt")
@@ -259,6 +265,8 @@ def main() -> int:
     rec["query"] = qres
     if c4 is not None:
         rec["c4_stream"] = c4
+    if c5 is not None:
+        rec["c5_long"] = c5
     if ext is not None:
         rec["extensions"] = ext
     print(json.dumps(rec), flush=True)
@@ -331,6 +339,62 @@ def _stream_flops(wl) -> float:
         t0 = min(s * C, M)
         pairs += wl.n_layers * wl.n_q_heads * (C * t0 + C * (C + 1) // 2)
     return 4.0 * d * pairs
+
+
+def c5_bench(steps: int, warmup: int) -> dict:
+    """The long-cache configuration of the 7B shape: 32768 cached + 3136 new
+    tokens per layer (budgets 4096..16384), one append + compress per step
+    with the cache rewound between steps, then the 64-token query over the
+    compacted caches."""
+    import concurrent.futures as cf
+
+    import torch
+
+    from paper_2601_14724_amd import hermes as H
+    from paper_2601_14724_amd import streaming, workloads as wk
+    wl = wk.WORKLOADS["c5_7b_long"]
+    with cf.ThreadPoolExecutor(max_workers=8) as ex:
+        caches = list(ex.map(lambda l: wk.gen_cache(wl, l), range(wl.n_layers)))
+        chunks = list(ex.map(lambda l: wk.gen_chunk(wl, 0, l), range(wl.n_layers)))
+    kv = streaming.make_cache(wl, device="cuda:0", caches=caches)
+    st = {k: np.stack([c[k] for c in chunks]) for k in ("q", "k", "v")} | {"pos": chunks[0]["pos"]}
+    t = streaming.chunk_tensors(st, "cuda:0")
+    out = torch.empty_like(t["q"])
+    del caches, chunks, st
+
+    def step():
+        kv.rewind()
+        kv.append(t["q"], t["k"], t["v"], t["pos"], out=out)
+        kv.compress()
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    kv.profile(True)
+    for kid in range(len(H.KERNEL_NAMES)):
+        kv.profile_read(kid)
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    kernels = {}
+    for kid, name in enumerate(H.KERNEL_NAMES):
+        ms, cnt = kv.profile_read(kid)
+        if cnt:
+            kernels[name] = round(ms / steps, 4)
+    kv.profile(False)
+    fl = attention_flops(wl)
+    att_tf = fl / (kernels["attention"] * 1e-3) / 1e12
+    res = {"workload": wl.name, "steps": steps, "ms_per_step": round(1e3 * elapsed / steps, 4),
+           "video_tokens_per_s": round(wl.chunk * steps / elapsed, 1), "kernels_ms": kernels,
+           "attention_TFLOPs": round(att_tf, 2), "attention_mfma_frac": round(att_tf / PEAK_BF16_TFLOPS, 4),
+           "query": query_bench(wl, kv, steps, warmup)}
+    kv.close()
+    return res
 
 
 def query_bench(wl, kv, steps: int, warmup: int, n_q: int = 64) -> dict:
