@@ -79,11 +79,21 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
   // Consecutive ids: the query tiles of one (layer, KV head[, key slice]),
   // which stream the same K/V.
-  const int nsp = SPLIT ? a.nsplit : 1;
-  const int qtile = lin % nqt;
-  const int split = SPLIT ? (lin / nqt) % nsp : 0;
-  const int kv = SPLIT ? (lin / (nqt * nsp)) % a.Hkv : (lin / nqt) % a.Hkv;
-  const int j = SPLIT ? lin / (nqt * nsp * a.Hkv) : lin / (nqt * a.Hkv);
+  int j, qtile, kv, split = 0, nsp = 1;
+  if constexpr (SPLIT) {
+    // entry j owns workgroups [wg_start[j], wg_start[j+1]) (uniform search)
+    j = 0;
+    while (j + 1 < kMaxLayers && lin >= a.wg_start[j + 1]) ++j;
+    const int local = lin - a.wg_start[j];
+    nsp = a.nsp[j];
+    qtile = local % nqt;
+    split = (local / nqt) % nsp;
+    kv = local / (nqt * nsp);
+  } else {
+    qtile = lin % nqt;
+    kv = (lin / nqt) % a.Hkv;
+    j = lin / (nqt * a.Hkv);
+  }
   const int layer = a.layer_id[j];
   const LayerTable &lt = a.tab[layer];
   const int cur = a.cur[j];
@@ -355,7 +365,7 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   if constexpr (SPLIT) {
     // unnormalised partial state of this key slice
     if (row_ok) {
-      const int64_t row = ((int64_t)(j * Hkv + kv) * nsp + split) * a.part_rows + prow;
+      const int64_t row = ((int64_t)(j * Hkv + kv) * kMaxSplits + split) * a.part_rows + prow;
       float *op = a.opart + row * D;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
@@ -400,11 +410,11 @@ template <int D>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int j = blockIdx.z, kv = blockIdx.y;
   const int layer = a.layer_id[j];
-  const int G = a.Hq / a.Hkv, P = a.C * G, nsp = a.nsplit;
+  const int G = a.Hq / a.Hkv, P = a.C * G, nsp = a.nsp[j];
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= P * (D / 8)) return;
   const int p = e / (D / 8), c8 = e % (D / 8);
-  const int64_t row0 = (int64_t)(j * a.Hkv + kv) * nsp * a.part_rows + p;
+  const int64_t row0 = (int64_t)(j * a.Hkv + kv) * kMaxSplits * a.part_rows + p;
   float m = -INFINITY;
   for (int s = 0; s < nsp; ++s) m = fmaxf(m, a.mlpart[2 * (row0 + (int64_t)s * a.part_rows)]);
   float lsum = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -685,7 +695,7 @@ hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStre
 hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, hipStream_t s) {
   const int P = a.C * (a.Hq / a.Hkv);
   const int nqt = (P + BM - 1) / BM;
-  dim3 grid(nqt * a.nsplit * a.Hkv * n_list);
+  dim3 grid(a.wg_start[n_list]);
   dim3 cgrid((P * (head_dim / 8) + 255) / 256, a.Hkv, n_list);
   if (head_dim == 64) {
     hipLaunchKernelGGL((attn_fwd<64, true, true>), grid, dim3(AT), 0, s, a, nqt);

@@ -131,20 +131,60 @@ Layout layout_of(const hermes_config *c) {
   return s;
 }
 
-// Key slices for a pass of n_rows rows over caches of at most max_T0 tokens:
-// as many as keep all workgroups in one round of the GPU's slots (one
-// attention workgroup on each of 256 CUs), each slice at least 8 key tiles;
-// 1 means the plain kernel.  A second round would repeat every workgroup's
-// fixed cost (query load, partial-state write) for no gain in parallelism.
-int split_count(int n_rows, int G, int Hkv, int n_list, int max_T0) {
-  if (n_rows > kSplitMaxTokens) return 1;
+// Key slices of a short pass (n_rows <= kSplitMaxTokens rows per entry over
+// caches of at.T0[j] tokens): entry j's key tiles are cut into nsp[j] slices
+// of at most m tiles (at least 8 tiles, at most kMaxSplits slices), with the
+// m that minimises rounds(m) * (longest slice + fixed work) + the combine's
+// cost, where rounds(m) is the number of 256-workgroup rounds (one attention
+// workgroup per CU) the slices take; slicing is used only when it promises at
+// least 10% over the plain kernel.  Without slicing, one workgroup per
+// (entry, KV head, query tile) runs over its whole cache, so the entry with
+// the longest cache sets the time while the others' CUs idle.  Fills nsp,
+// wg_start and nsplit (the largest nsp; 1 means the plain kernel).
+void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
   const int nqt = (n_rows * G + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
-  const int base = nqt * Hkv * n_list;
-  const int want = 256 / base;
-  const int tiles = (max_T0 + n_rows + 63) / 64;
-  int s = want < kMaxSplits ? want : kMaxSplits;
-  if (s > tiles / 8) s = tiles / 8;
-  return s < 1 ? 1 : s;
+  std::vector<int> tiles(n_list);
+  int max_tiles = 1;
+  for (int j = 0; j < n_list; ++j) {
+    tiles[j] = (at.T0[j] + n_rows + 63) / 64;
+    max_tiles = tiles[j] > max_tiles ? tiles[j] : max_tiles;
+  }
+  // Costs in key-tile times: a round of workgroups also pays about two tiles
+  // of fixed work (query load, epilogue); slices add the combine launch and
+  // the write and read of each workgroup's fp32 partial O (about one tile per
+  // 32 * 128 / D workgroups).
+  auto rounds = [](int64_t w) { return (double)((w + 255) / 256); };
+  double best = 0.9 * rounds((int64_t)nqt * Hkv * n_list) * (max_tiles + 2.0);
+  int best_m = 0;
+  if (n_rows <= kSplitMaxTokens) {
+    for (int m = 8; m < max_tiles; ++m) {
+      int64_t w = 0;
+      int longest = 0, most = 1;
+      for (int j = 0; j < n_list; ++j) {
+        int ns = (tiles[j] + m - 1) / m;
+        ns = ns < kMaxSplits ? ns : kMaxSplits;
+        most = ns > most ? ns : most;
+        w += (int64_t)nqt * Hkv * ns;
+        const int len = (tiles[j] + ns - 1) / ns;
+        longest = len > longest ? len : longest;
+      }
+      if (most == 1) continue;
+      const double cost = rounds(w) * (longest + 2.0) + 2.0 + (double)w * D / (32.0 * 128.0);
+      if (cost < best) {
+        best = cost;
+        best_m = m;
+      }
+    }
+  }
+  at.nsplit = 1;
+  at.wg_start[0] = 0;
+  for (int j = 0; j < n_list; ++j) {
+    int ns = best_m > 0 ? (tiles[j] + best_m - 1) / best_m : 1;
+    ns = ns < kMaxSplits ? ns : kMaxSplits;
+    at.nsp[j] = (int8_t)ns;
+    at.nsplit = ns > at.nsplit ? ns : at.nsplit;
+    at.wg_start[j + 1] = at.wg_start[j] + nqt * Hkv * ns;
+  }
 }
 
 // 10% shallow, 60% middle, 30% deep (Sec. 4.1), rounded to nearest layer.
@@ -744,7 +784,7 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
     max_T = ctx->len[l] > max_T ? ctx->len[l] : max_T;
   }
   const int n = (int)list.size();
-  at.nsplit = split_count(n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, max_T);
+  split_plan(at, n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D);
   at.part_rows = ctx->lay.part_rows;
   at.opart = reinterpret_cast<float *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
@@ -978,17 +1018,16 @@ int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   at.Hkv = ctx->Hkv;
   at.C = n_q;
   at.scale_log2 = (float)(ctx->sm_scale * kLog2e);
-  int n = 0, max_T0 = 0;
+  int n = 0;
   for (int l = 0; l < L; ++l) {
     if (layer != HERMES_ALL_LAYERS && l != layer) continue;
     at.T0[n] = ctx->len[l];
     at.layer_id[n] = (int8_t)l;
     at.slot[n] = (int8_t)(layer == HERMES_ALL_LAYERS ? l : 0);
     at.cur[n] = ctx->cur[l];
-    max_T0 = ctx->len[l] > max_T0 ? ctx->len[l] : max_T0;
     ++n;
   }
-  at.nsplit = split_count(n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, max_T0);
+  split_plan(at, n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D);
   at.part_rows = ctx->lay.part_rows;
   at.opart = reinterpret_cast<float *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);

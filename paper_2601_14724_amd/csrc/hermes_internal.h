@@ -46,11 +46,14 @@ struct AttnArgs {
   int8_t layer_id[kMaxLayers];
   int8_t slot[kMaxLayers];      // index of the layer's inputs in the stacked tensors
   int8_t cur[kMaxLayers];
-  // Split-key mode (short passes): each workgroup covers one of nsplit slices
-  // of the key tiles and writes unnormalised O, the running maximum and the
-  // row sum to opart / mlpart [entry][Hkv][nsplit][part_rows]; a combine
-  // kernel merges the slices.
+  // Split-key mode (short passes): entry j's key tiles are cut into nsp[j]
+  // slices (at most kMaxSplits; nsplit is the largest), workgroups
+  // [wg_start[j], wg_start[j+1]) cover entry j, and each writes unnormalised
+  // O, the running maximum and the row sum of its slice to opart / mlpart
+  // [entry][Hkv][kMaxSplits][part_rows]; a combine kernel merges the slices.
   int32_t nsplit, part_rows;
+  int8_t nsp[kMaxLayers];
+  int32_t wg_start[kMaxLayers + 1];
   float *opart;             // [..][part_rows][d] fp32
   float *mlpart;            // [..][part_rows][2] fp32 (max, sum)
 };
@@ -234,7 +237,7 @@ constexpr int kAttnRowsPerBlock = 256;   // packed (row, head) pairs per attenti
 constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the sweep
 constexpr int kSummaryRows = 128;        // candidates per workgroup of the summary sums
 constexpr int kSplitMaxTokens = 64;      // passes of at most this many rows use split keys
-constexpr int kMaxSplits = 4;
+constexpr int kMaxSplits = 8;
 constexpr int kNormBlock = 256;         // candidates per fp64 partial of the score normaliser
 
 }  // namespace hermes
