@@ -145,3 +145,30 @@ def test_long_layers_past_the_lds_staging_limits():
     one wave loads at once."""
     wl = wk.custom("long", 123, 2, 2, 1, 64, 40000, 32, [20000, 30000])
     _step_parity(wl, classes=[orc.MIDDLE, orc.DEEP])
+
+
+def test_query_with_per_layer_key_slices():
+    """Layers of very different cache lengths (300, 2000 and 8000 tokens): the
+    host cuts their keys into 1, 2 and 8 slices (the most it allows), whose
+    partial states the combine merges; each layer's query output against the
+    oracle's attention over that layer's cache."""
+    from paper_2601_14724_amd import streaming
+    wl = wk.custom("slices", 123, 3, 4, 2, 64, 8000, 9, (8000, 8000, 8000), query_len=9)
+    lens = (300, 2000, 8000)
+    caches = []
+    for l in range(wl.n_layers):
+        c = wk.gen_cache(wl, l)
+        caches.append({k: np.ascontiguousarray(c[k][:lens[l]]) for k in ("k", "v", "pos")})
+    kv = streaming.make_cache(wl, caches=caches)
+    assert [kv.length(l) for l in range(wl.n_layers)] == list(lens)
+    qry = [wk.gen_query(wl, l) for l in range(wl.n_layers)]
+    qt = {k: streaming.bf16_tensor(np.stack([x[k] for x in qry]), "cuda") for k in ("q", "k", "v")}
+    o = kv.query(qt["q"], qt["k"], qt["v"]).float().cpu().numpy()
+    f64 = wk.bf16_bits_to_f64
+    for l in range(wl.n_layers):
+        cache = orc.LayerCache(f64(caches[l]["k"]), f64(caches[l]["v"]),
+                               caches[l]["pos"].astype(np.int64))
+        want = orc.query_attention(cache, f64(qry[l]["q"]), f64(qry[l]["k"]), f64(qry[l]["v"]))
+        err = np.abs(o[l] - want).max()
+        assert err <= 2e-2, (l, err)
+    kv.close()
