@@ -157,7 +157,9 @@ void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
   double best = 0.9 * rounds((int64_t)nqt * Hkv * n_list) * (max_tiles + 2.0);
   int best_m = 0;
   if (n_rows <= kSplitMaxTokens) {
-    for (int m = 8; m < max_tiles; ++m) {
+    // every slice length up to 64 tiles, then steps of m / 16 (a few hundred
+    // candidates even for million-token caches)
+    for (int m = 8; m < max_tiles; m += m < 64 ? 1 : m / 16) {
       int64_t w = 0;
       int longest = 0, most = 1;
       for (int j = 0; j < n_list; ++j) {
