@@ -366,14 +366,17 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
     // unnormalised partial state of this key slice
     if (row_ok) {
       const int64_t row = ((int64_t)(j * Hkv + kv) * kMaxSplits + split) * a.part_rows + prow;
-      float *op = a.opart + row * D;
+      // bf16 halves the state the combine reads back; the maximum and the
+      // row sum, which fix the LSE, stay fp32
+      uint16_t *op = a.opart + row * D;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
 #pragma unroll
         for (int grp = 0; grp < 4; ++grp) {
           const int d0 = 32 * db + 8 * grp + 4 * half;
-          *reinterpret_cast<float4 *>(op + d0) =
-              float4{o[db][4 * grp], o[db][4 * grp + 1], o[db][4 * grp + 2], o[db][4 * grp + 3]};
+          const uint32_t w0 = (uint32_t)f2bf(o[db][4 * grp + 0]) | ((uint32_t)f2bf(o[db][4 * grp + 1]) << 16);
+          const uint32_t w1 = (uint32_t)f2bf(o[db][4 * grp + 2]) | ((uint32_t)f2bf(o[db][4 * grp + 3]) << 16);
+          *reinterpret_cast<uint2 *>(op + d0) = uint2{w0, w1};
         }
       if (half == 0) *reinterpret_cast<float2 *>(a.mlpart + 2 * row) = float2{m_run, l_tot};
     }
@@ -422,10 +425,13 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
     const int64_t row = row0 + (int64_t)s * a.part_rows;
     const float w = exp2f(a.mlpart[2 * row] - m);
     lsum += w * a.mlpart[2 * row + 1];
-    const float4 x0 = *reinterpret_cast<const float4 *>(a.opart + row * D + 8 * c8);
-    const float4 x1 = *reinterpret_cast<const float4 *>(a.opart + row * D + 8 * c8 + 4);
-    acc[0] += w * x0.x; acc[1] += w * x0.y; acc[2] += w * x0.z; acc[3] += w * x0.w;
-    acc[4] += w * x1.x; acc[5] += w * x1.y; acc[6] += w * x1.z; acc[7] += w * x1.w;
+    const uint4 x = *reinterpret_cast<const uint4 *>(a.opart + row * D + 8 * c8);
+    const uint32_t xw[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      acc[2 * i] += w * __uint_as_float(xw[i] << 16);
+      acc[2 * i + 1] += w * __uint_as_float(xw[i] & 0xffff0000u);
+    }
   }
   const int r = p / G, h = kv * G + (p - r * G);
   if (a.out != nullptr) {

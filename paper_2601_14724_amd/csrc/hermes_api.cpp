@@ -124,7 +124,7 @@ Layout layout_of(const hermes_config *c) {
   s.part_rows = kSplitMaxTokens * (c->n_q_heads / c->n_kv_heads);
   const size_t prow = (size_t)c->n_layers * c->n_kv_heads * kMaxSplits * s.part_rows;
   s.opart = off;
-  off = round_up(off + sizeof(float) * prow * c->head_dim);
+  off = round_up(off + sizeof(uint16_t) * prow * c->head_dim);
   s.mlpart = off;
   off = round_up(off + sizeof(float) * prow * 2);
   s.total = off;
@@ -151,8 +151,8 @@ void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
   }
   // Costs in key-tile times: a round of workgroups also pays about two tiles
   // of fixed work (query load, epilogue); slices add the combine launch and
-  // the write and read of each workgroup's fp32 partial O (about one tile per
-  // 32 * 128 / D workgroups).
+  // the write and read of each workgroup's bf16 partial O (about one tile per
+  // 64 * 128 / D workgroups).
   auto rounds = [](int64_t w) { return (double)((w + 255) / 256); };
   double best = 0.9 * rounds((int64_t)nqt * Hkv * n_list) * (max_tiles + 2.0);
   int best_m = 0;
@@ -171,7 +171,7 @@ void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
         longest = len > longest ? len : longest;
       }
       if (most == 1) continue;
-      const double cost = rounds(w) * (longest + 2.0) + 2.0 + (double)w * D / (32.0 * 128.0);
+      const double cost = rounds(w) * (longest + 2.0) + 2.0 + (double)w * D / (64.0 * 128.0);
       if (cost < best) {
         best = cost;
         best_m = m;
@@ -788,7 +788,7 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
   const int n = (int)list.size();
   split_plan(at, n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D);
   at.part_rows = ctx->lay.part_rows;
-  at.opart = reinterpret_cast<float *>(ctx->ws + ctx->lay.opart);
+  at.opart = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
   const int rc = ctx->run(HERMES_K_GUIDE, s, [&] {
     hipError_t e = at.nsplit > 1 ? launch_attention_split(at, n, ctx->D, s)
@@ -1031,7 +1031,7 @@ int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const voi
   }
   split_plan(at, n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D);
   at.part_rows = ctx->lay.part_rows;
-  at.opart = reinterpret_cast<float *>(ctx->ws + ctx->lay.opart);
+  at.opart = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
   return ctx->run(HERMES_K_QUERY, s, [&] {
     return at.nsplit > 1 ? launch_attention_split(at, n, ctx->D, s)

@@ -49,12 +49,12 @@ struct AttnArgs {
   // Split-key mode (short passes): entry j's key tiles are cut into nsp[j]
   // slices (at most kMaxSplits; nsplit is the largest), workgroups
   // [wg_start[j], wg_start[j+1]) cover entry j, and each writes unnormalised
-  // O, the running maximum and the row sum of its slice to opart / mlpart
+  // O (bf16), the running maximum and the row sum (fp32) of its slice to opart / mlpart
   // [entry][Hkv][kMaxSplits][part_rows]; a combine kernel merges the slices.
   int32_t nsplit, part_rows;
   int8_t nsp[kMaxLayers];
   int32_t wg_start[kMaxLayers + 1];
-  float *opart;             // [..][part_rows][d] fp32
+  uint16_t *opart;          // [..][part_rows][d] bf16 (unnormalised; its scale is in mlpart)
   float *mlpart;            // [..][part_rows][2] fp32 (max, sum)
 };
 
