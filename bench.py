@@ -83,8 +83,28 @@ def attn_traffic(wl):
     return ATTN_TRAFFIC["bytes"]
 
 
+def _cpu_model() -> str:
+    """The host CPU's model name (lscpu, else /proc/cpuinfo)."""
+    import subprocess
+    try:
+        out = subprocess.run(["lscpu"], capture_output=True, text=True, timeout=10).stdout
+        for line in out.splitlines():
+            if line.startswith("Model name:"):
+                return line.split(":", 1)[1].strip()
+    except (OSError, subprocess.SubprocessError):
+        pass
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
 def cpu_baseline(wl, n_layers: int) -> dict:
-    from threadpoolctl import threadpool_info
+    from threadpoolctl import threadpool_info, threadpool_limits
 
     from oracle import hermes_oracle as orc
     from paper_2601_14724_amd import workloads as wk
@@ -97,16 +117,21 @@ def cpu_baseline(wl, n_layers: int) -> dict:
     classes = orc.layer_partition(wl.n_layers)[:n_layers]
     cfg = orc.OracleConfig(budgets=list(wl.budgets[:n_layers]), classes=classes,
                            lambdas=orc.smoothing_lambdas(orc.layer_partition(wl.n_layers))[:n_layers])
-    t0 = time.perf_counter()
-    orc.stream_step(oc, och, cfg)
-    dt = time.perf_counter() - t0
-    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    # the oracle's BLAS calls run on every core this process may use
+    affinity = len(os.sched_getaffinity(0))
+    with threadpool_limits(affinity):
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        t0 = time.perf_counter()
+        orc.stream_step(oc, och, cfg)
+        dt = time.perf_counter() - t0
     per_step = dt * wl.n_layers / n_layers
-    return {"value": wl.chunk / per_step, "unit": "video tokens/s", "cores": int(threads),
-            "kind": "oracle",
+    return {"value": wl.chunk / per_step, "unit": "video tokens/s", "cores": int(min(threads, affinity)),
+            "kind": "oracle", "affinity_cores": affinity, "host_cpus": os.cpu_count(),
+            "cpu_model": _cpu_model(),
             "sample": f"fp64 oracle step (attention+mass, scoring, smoothing, top-k, gather) on "
                       f"layers 0..{n_layers - 1} of the 28-layer workload, {dt:.1f} s, scaled "
-                      f"x{wl.n_layers}/{n_layers} to the whole step"}
+                      f"x{wl.n_layers}/{n_layers} to the whole step; matrix products on "
+                      f"{min(threads, affinity)} BLAS threads, element-wise work on one"}
 
 
 def main() -> int:

@@ -607,7 +607,38 @@ __global__ __launch_bounds__(NT) void score_keys(SelectArgs a) {
 
 }
 
-// 2. TopK of each listed layer from its keys (staged in LDS when they fit).
+// TopK of keys[0..T) (M < T) into out (and out2 if non-null): staged in LDS
+// when they fit, held in registers for the radix passes when T <= kRegKeys
+// * NT, read from global memory (L2-resident) otherwise.  Shared by the
+// compression and the stand-alone entry point.
+__device__ __forceinline__ void select_keys(const uint32_t *keys, int T, int M, int32_t *out, int32_t *out2,
+                                            SelectShared &sh, uint32_t *big) {
+  if (T <= kLdsKeys) {
+    stage_u32<NT, 10>(keys, T, big);
+    __syncthreads();
+    if (T <= kRegKeys * NT) {
+      // keys in registers: big is free once the radix passes are done and
+      // takes the kept list, written out coalesced
+      select_top_regs<kRegKeys>(big, T, M, reinterpret_cast<int32_t *>(big), nullptr, sh);
+      __syncthreads();
+#pragma unroll
+      for (int u = 0; u < kRegKeys; ++u) {
+        const int i = u * NT + threadIdx.x;
+        if (i < M) {   // M < T <= kRegKeys * NT
+          const int32_t x = static_cast<int32_t>(big[i]);
+          out[i] = x;
+          if (out2 != nullptr) out2[i] = x;
+        }
+      }
+    } else {
+      select_top(static_cast<const uint32_t *>(big), T, M, out, out2, sh);
+    }
+  } else {
+    select_top(keys, T, M, out, out2, sh);
+  }
+}
+
+// 2. TopK of each listed layer from its keys.
 __global__ __launch_bounds__(NT) void select_kept(SelectArgs a) {
   __shared__ SelectShared sh;
   __shared__ uint32_t big[kLdsKeys];
@@ -615,40 +646,18 @@ __global__ __launch_bounds__(NT) void select_kept(SelectArgs a) {
   const LayerTable &L0 = a.tab[l];
   const int T = a.len[l];
   if (T <= L0.budget) return;
-  const uint32_t *keys = a.keys + l * a.keys_lstride;
-  int32_t *kept = a.kept + l * a.kept_lstride;
-  if (T <= kLdsKeys) {
-    stage_u32<NT, 10>(keys, T, big);
-    __syncthreads();
-    if (T <= kRegKeys * NT) {
-      // keys in registers: big is free once the radix passes are done and
-      // takes the kept list, written out coalesced
-      select_top_regs<kRegKeys>(big, T, L0.budget, reinterpret_cast<int32_t *>(big), nullptr, sh);
-      __syncthreads();
-      const int M = L0.budget;   // < T <= kRegKeys * NT
-#pragma unroll
-      for (int u = 0; u < kRegKeys; ++u) {
-        const int i = u * NT + threadIdx.x;
-        if (i < M) {
-          const int32_t x = static_cast<int32_t>(big[i]);
-          kept[i] = x;
-          if (L0.kept_dbg != nullptr) L0.kept_dbg[i] = x;
-        }
-      }
-    }
-    else select_top(static_cast<const uint32_t *>(big), T, L0.budget, kept, L0.kept_dbg, sh);
-  } else {
-    select_top(keys, T, L0.budget, kept, L0.kept_dbg, sh);
-  }
+  select_keys(a.keys + l * a.keys_lstride, T, L0.budget, a.kept + l * a.kept_lstride, L0.kept_dbg, sh,
+              big);
 }
 
 __global__ __launch_bounds__(NT) void topk_keys(const uint32_t *keys, int n, int k, int32_t *out) {
   __shared__ SelectShared sh;
+  __shared__ uint32_t big[kLdsKeys];
   if (k >= n) {
     for (int i = threadIdx.x; i < n; i += NT) out[i] = i;
     return;
   }
-  select_top(keys, n, k, out, nullptr, sh);
+  select_keys(keys, n, k, out, nullptr, sh, big);
 }
 
 }  // namespace

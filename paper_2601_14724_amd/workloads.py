@@ -18,7 +18,8 @@ Generation recipe (per tensor):
     tensor ids: chunk Q=0, chunk K=1, chunk V=2, cache K=3, cache V=4,
     low-rank basis U=5, chunk low-rank coefficients=6, cache coefficients=7,
     query Q=8, query K=9, query V=10, guidance-prompt Q=11, K=12, V=13 (step
-    id 1000 for the global prompt, 1001 for the hybrid local + global one);
+    id 1000 for the global prompt, 1001 for the hybrid local + global one),
+    anchor direction=14, anchor strengths=15, anchor value signs=16;
   * draw float64 N(0,1), scale by 0.5 (standard deviation 0.5);
   * the low-rank key workload adds 1.0 * (z @ U), U in R^{8 x d} with entries
     N(0, 1/8) per (layer, kv head) and z ~ N(0, I_8) per token, before scaling
@@ -27,6 +28,19 @@ Generation recipe (per tensor):
     inv_freq_j = theta^(-2j/d)) applied in float64 to Q and K at the token's
     stream position;  V gets none;
   * cast to float32, then to bfloat16 by round-to-nearest-even.
+
+Sharp-attention variant (anchor_period > 0), for checks whose attention
+outputs must be far above the rounding noise: every token whose stream
+position is a multiple of anchor_period is an anchor.  Per (layer, kv head) a
+unit direction u lives on the four lowest-frequency rotary pairs (RoPE turns
+it by at most a few hundredths of a radian over the workloads' spans), drawn
+once from tensor id 14 at step 0.  An anchor key gets + a_p * u with a_p =
+d^(1/4) * U(1, 5) (tensor id 15, drawn per anchor from its own position), an
+anchor value gets + 0.5 * (a random sign per element, tensor id 16); every
+query row (chunk, text query, guidance prompt) of query head h gets
++ 3 d^(1/4) * u of its kv head.  Scores of anchors then stand 3..15 above the
+rest (in units of the softmax exponent), so a few anchors spread over the
+cache dominate each row and |O| is of order 0.5.  Added before RoPE.
 
 bfloat16 tensors are returned as numpy uint16 bit patterns so that the two
 consumers can view them without a conversion step of their own.
@@ -46,6 +60,7 @@ T_CACHE_K, T_CACHE_V = 3, 4
 T_LOWRANK_U, T_CHUNK_Z, T_CACHE_Z = 5, 6, 7
 T_QUERY_Q, T_QUERY_K, T_QUERY_V = 8, 9, 10
 T_PROMPT_Q, T_PROMPT_K, T_PROMPT_V = 11, 12, 13
+T_ANCHOR_U, T_ANCHOR_A, T_ANCHOR_V = 14, 15, 16
 PROMPT_GLOBAL, PROMPT_HYBRID = 0, 1
 
 
@@ -66,6 +81,7 @@ class Workload:
     query_len: int = 0       # text-query tokens attending the compact cache
     low_rank_keys: bool = False
     scale: float = 0.5
+    anchor_period: int = 0   # > 0: sharp-attention variant (planted anchor tokens)
 
     @property
     def group(self) -> int:
@@ -146,6 +162,48 @@ def _gauss(rng: np.random.Generator, shape, scale: float) -> np.ndarray:
     return rng.standard_normal(shape) * scale
 
 
+def _anchor_dir(wl: Workload, layer: int) -> np.ndarray:
+    """[Hkv][d] unit directions on the four lowest-frequency rotary pairs."""
+    d, half = wl.head_dim, wl.head_dim // 2
+    cols = np.concatenate([np.arange(half - 4, half), np.arange(d - 4, d)])
+    u = np.zeros((wl.n_kv_heads, d))
+    u[:, cols] = _rng(wl, 0, layer, T_ANCHOR_U).standard_normal((wl.n_kv_heads, cols.size))
+    return u / np.linalg.norm(u, axis=1, keepdims=True)
+
+
+def _is_anchor(wl: Workload, positions: np.ndarray) -> np.ndarray:
+    return (positions % wl.anchor_period) == 0
+
+
+def _anchor_keys(wl: Workload, layer: int, positions: np.ndarray, k: np.ndarray) -> np.ndarray:
+    if wl.anchor_period <= 0:
+        return k
+    u = _anchor_dir(wl, layer)
+    q4 = wl.head_dim ** 0.25
+    k = k.copy()
+    for i in np.nonzero(_is_anchor(wl, positions))[0]:
+        a = q4 * _rng(wl, int(positions[i]), layer, T_ANCHOR_A).uniform(1.0, 5.0, wl.n_kv_heads)
+        k[i] += a[:, None] * u
+    return k
+
+
+def _anchor_values(wl: Workload, layer: int, positions: np.ndarray, v: np.ndarray) -> np.ndarray:
+    if wl.anchor_period <= 0:
+        return v
+    v = v.copy()
+    for i in np.nonzero(_is_anchor(wl, positions))[0]:
+        sgn = _rng(wl, int(positions[i]), layer, T_ANCHOR_V).integers(0, 2, v.shape[1:]) * 2 - 1
+        v[i] += 0.5 * sgn
+    return v
+
+
+def _anchor_queries(wl: Workload, layer: int, q: np.ndarray) -> np.ndarray:
+    if wl.anchor_period <= 0:
+        return q
+    u = _anchor_dir(wl, layer)
+    return q + 3.0 * wl.head_dim ** 0.25 * np.repeat(u, wl.group, axis=0)[None]
+
+
 def _keys(wl: Workload, step: int, layer: int, n: int, noise_id: int, coef_id: int,
           positions: np.ndarray) -> np.ndarray:
     shape = (n, wl.n_kv_heads, wl.head_dim)
@@ -155,7 +213,7 @@ def _keys(wl: Workload, step: int, layer: int, n: int, noise_id: int, coef_id: i
             (wl.n_kv_heads, 8, wl.head_dim)) * np.sqrt(1.0 / 8.0)
         z = _rng(wl, step, layer, coef_id).standard_normal((n, wl.n_kv_heads, 8))
         k = k + 1.0 * np.einsum("nhr,hrd->nhd", z, basis)
-    return rope_f64(k, positions)
+    return rope_f64(_anchor_keys(wl, layer, positions, k), positions)
 
 
 def _to_bits(x: np.ndarray) -> np.ndarray:
@@ -168,6 +226,7 @@ def gen_cache(wl: Workload, layer: int) -> dict:
     pos = np.arange(n, dtype=np.int32)
     k = _keys(wl, 0, layer, n, T_CACHE_K, T_CACHE_Z, pos)
     v = _gauss(_rng(wl, 0, layer, T_CACHE_V), (n, wl.n_kv_heads, wl.head_dim), wl.scale)
+    v = _anchor_values(wl, layer, pos, v)
     return {"k": _to_bits(k), "v": _to_bits(v), "pos": pos}
 
 
@@ -175,10 +234,11 @@ def gen_chunk(wl: Workload, step: int, layer: int) -> dict:
     """The chunk appended to `layer` at `step`: Q, K, V and positions."""
     n = wl.chunk
     pos = wl.chunk_positions(step)
-    q = rope_f64(_gauss(_rng(wl, step, layer, T_CHUNK_Q), (n, wl.n_q_heads, wl.head_dim),
-                        wl.scale), pos)
+    q = rope_f64(_anchor_queries(wl, layer, _gauss(_rng(wl, step, layer, T_CHUNK_Q),
+                                                   (n, wl.n_q_heads, wl.head_dim), wl.scale)), pos)
     k = _keys(wl, step, layer, n, T_CHUNK_K, T_CHUNK_Z, pos)
     v = _gauss(_rng(wl, step, layer, T_CHUNK_V), (n, wl.n_kv_heads, wl.head_dim), wl.scale)
+    v = _anchor_values(wl, layer, pos, v)
     return {"q": _to_bits(q), "k": _to_bits(k), "v": _to_bits(v), "pos": pos}
 
 
@@ -186,8 +246,8 @@ def gen_query(wl: Workload, layer: int) -> dict:
     """The text query's Q/K/V for `layer`, placed after the whole stream."""
     n = wl.query_len
     pos = wl.query_positions()
-    q = rope_f64(_gauss(_rng(wl, 0, layer, T_QUERY_Q), (n, wl.n_q_heads, wl.head_dim),
-                        wl.scale), pos)
+    q = rope_f64(_anchor_queries(wl, layer, _gauss(_rng(wl, 0, layer, T_QUERY_Q),
+                                                   (n, wl.n_q_heads, wl.head_dim), wl.scale)), pos)
     k = rope_f64(_gauss(_rng(wl, 0, layer, T_QUERY_K), (n, wl.n_kv_heads, wl.head_dim),
                         wl.scale), pos)
     v = _gauss(_rng(wl, 0, layer, T_QUERY_V), (n, wl.n_kv_heads, wl.head_dim), wl.scale)
@@ -203,8 +263,8 @@ def gen_prompt(wl: Workload, layer: int, n_rows: int, kind: int = PROMPT_GLOBAL,
         start = wl.init_len + wl.chunk
     pos = np.arange(start, start + n_rows, dtype=np.int32)
     step = 1000 + kind
-    q = rope_f64(_gauss(_rng(wl, step, layer, T_PROMPT_Q), (n_rows, wl.n_q_heads, wl.head_dim),
-                        wl.scale), pos)
+    q = rope_f64(_anchor_queries(wl, layer, _gauss(_rng(wl, step, layer, T_PROMPT_Q),
+                                                   (n_rows, wl.n_q_heads, wl.head_dim), wl.scale)), pos)
     k = rope_f64(_gauss(_rng(wl, step, layer, T_PROMPT_K), (n_rows, wl.n_kv_heads, wl.head_dim),
                         wl.scale), pos)
     v = _gauss(_rng(wl, step, layer, T_PROMPT_V), (n_rows, wl.n_kv_heads, wl.head_dim), wl.scale)
@@ -219,10 +279,10 @@ def scaled(wl: Workload, **changes) -> Workload:
 def custom(name: str, workload_id: int, n_layers: int, n_q_heads: int, n_kv_heads: int,
            head_dim: int, init_len: int, chunk: int, budgets: Sequence[int], n_steps: int = 1,
            query_len: int = 0, low_rank_keys: bool = False,
-           scale: float = 0.5) -> Workload:
+           scale: float = 0.5, anchor_period: int = 0) -> Workload:
     return Workload(name, workload_id, n_layers, n_q_heads, n_kv_heads, head_dim, init_len,
                     chunk, n_steps, tuple(int(b) for b in budgets), query_len, low_rank_keys,
-                    scale)
+                    scale, anchor_period)
 
 
 def stack_chunks(wl: Workload, step: int, layers: Optional[Sequence[int]] = None,

@@ -2,7 +2,10 @@
 C ABI and through the fp64 oracle on the same seeded inputs, and compare to
 the tolerances of the streaming-step contract:
 
-  * attention outputs within max-abs 2e-2 (bf16 inputs, fp32 accumulation);
+  * attention outputs within max-abs 2e-2 (bf16 inputs, fp32 accumulation),
+    and, so that the bar can fail where the outputs themselves are small
+    (long caches spread the softmax thin), within 2e-2 of max|O_ref| and
+    within 1e-2 relative in the L2 norm;
   * attention mass W and smoothed keys S~ within 1e-3 relative;
   * kept index sets bit-exact, except tokens whose oracle S~ lies within 1e-6
     relative of the budget-th largest;
@@ -19,6 +22,8 @@ from oracle import hermes_oracle as orc
 from paper_2601_14724_amd import streaming, workloads as wk
 
 O_ATOL = 2e-2
+O_RREL = 2e-2    # max |O - O_ref| / max |O_ref|
+O_L2REL = 1e-2   # ||O - O_ref||_2 / ||O_ref||_2
 W_RTOL = 1e-3
 S_RTOL = 1e-3
 BAND = 1e-6
@@ -29,6 +34,25 @@ f64 = wk.bf16_bits_to_f64
 def say(*a):
     print(*a, flush=True)
     sys.stdout.flush()
+
+
+def check_o(got, want, what):
+    """Attention output against the oracle: max-abs 2e-2 (the contract), plus
+    the two signal-relative bars, which an all-zero or a mis-normalised output
+    fails however small the outputs are.  Returns and prints the errors."""
+    got = np.asarray(got, dtype=np.float64)
+    want = np.asarray(want, dtype=np.float64)
+    assert got.shape == want.shape, (what, got.shape, want.shape)
+    diff = np.abs(got - want)
+    err = float(diff.max())
+    scale = float(np.abs(want).max())
+    rel = err / scale if scale > 0 else err
+    l2 = float(np.linalg.norm(got - want) / max(np.linalg.norm(want), 1e-300))
+    say(f"{what}: O max-abs {err:.3e} (max|O_ref| {scale:.3e}, rel {rel:.3e}), L2 rel {l2:.3e}")
+    assert err <= O_ATOL, f"{what}: attention max-abs {err}"
+    assert rel <= O_RREL, f"{what}: attention error {rel} of max|O_ref|"
+    assert l2 <= O_L2REL, f"{what}: attention L2 relative error {l2}"
+    return {"o_maxabs": err, "o_rel": rel, "o_l2rel": l2}
 
 
 def gen(wl, step=0, layers=None):
@@ -73,10 +97,7 @@ def band_of(st, budget):
 def check_layer(l, kv, out_gpu, w_gpu, ref, budget, chunk, check_w=True, check_s=True,
                 report=None):
     """Compare one layer of a GPU step with the oracle; returns error stats."""
-    stats = {}
-    err = float(np.abs(out_gpu[l] - ref["out"][l]).max())
-    stats["o_maxabs"] = err
-    assert err <= O_ATOL, f"layer {l}: attention max-abs {err}"
+    stats = check_o(out_gpu[l], ref["out"][l], f"layer {l}")
     T = ref["appended"][l].k.shape[0]
     if check_w:
         wr = ref["w"][l]

@@ -252,6 +252,19 @@ def _grid(frames, H, W, offset=0, t_step=1):
     return np.array(out, dtype=np.int64)
 
 
+@pytest.mark.parametrize("d,want", [(128, (16, 24, 24)), (64, (8, 12, 12)), (256, (32, 48, 48))])
+def test_default_mrope_section(d, want):
+    """The default split of the d/2 frequency pairs over (t, h, w): the
+    backbone's published M-RoPE section sizes, 16/24/24 pairs at head size
+    128 (the paper only names "the channel section allocated for dimension
+    d"), i.e. a quarter of the pairs for t and the rest halved, contiguous in
+    the order t, h, w and covering every pair once."""
+    assert he.default_mrope_section(d) == want
+    axis = he.mrope_pair_axis(d, want)
+    assert len(axis) == d // 2 and np.all(np.diff(axis) >= 0)
+    assert [int((axis == a).sum()) for a in range(3)] == list(want)
+
+
 def test_mrope_with_one_section_reduces_to_1d():
     """All pairs in the t section: the sectioned rotation is the 1D rotation
     by the t delta, and ranking strictly increasing t is the 1D rank."""
