@@ -125,10 +125,6 @@ typedef struct {
 
 /* Position re-indexing (Sec. 3.3; appendix, 1D RoPE re-indexing). */
 enum { HERMES_REINDEX_NONE = 0, HERMES_REINDEX_EAGER = 1, HERMES_REINDEX_LAZY = 2 };
-/* 3D re-indexing ranks the coordinates of one layer on one axis when they
- * span at most this many values (max - min + 1); a wider axis keeps its
- * coordinates, and the key sections it drives are not turned. */
-enum { HERMES_MROPE_MAX_SPAN = 262144 };
 /* Source of W: the chunk's own queries (default) or a guidance prompt used as
  * a pseudo-query (Sec. 3.1 deep-layer paragraph; appendix guidance prompts). */
 enum { HERMES_SCORE_CHUNK = 0, HERMES_SCORE_GUIDANCE = 1 };
@@ -330,11 +326,13 @@ void hermes_kv_destroy(hermes_ctx *ctx);
 const char *hermes_strerror(int code);
 
 /*
- * Stand-alone TopK (Sec. 3.2 TopK equation) over caller keys, with the same
- * kernel code the compression uses: keys is device fp32 [n] of non-negative
- * finite values, out_idx device int32 [k]; writes the k largest keys'
- * indices in ascending order, ties to the higher index.  k >= n writes
- * 0..n-1.  Errors: EINVAL (null pointer, n < 1, k < 1), EHIP.
+ * Stand-alone TopK (Sec. 3.2 TopK equation) over caller keys, through the
+ * selection routine the compression runs per layer (keys held in registers
+ * up to 10240 of them, staged in LDS up to 38400, read from memory beyond):
+ * keys is device fp32 [n] of non-negative finite values, out_idx device
+ * int32 [k]; writes the k largest keys' indices in ascending order, ties to
+ * the higher index.  k >= n writes 0..n-1.  One workgroup, no scratch memory.
+ * Errors: EINVAL (null pointer, n < 1, k < 1), EHIP.
  */
 int hermes_select_topk(const float *keys, int32_t n, int32_t k, int32_t *out_idx,
                        void *stream);

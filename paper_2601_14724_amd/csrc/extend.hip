@@ -46,13 +46,13 @@ __device__ __forceinline__ double bf16_to_f64(uint16_t b) {
   return (double)__builtin_bit_cast(float, (uint32_t)b << 16);
 }
 
+// fp64 -> fp32 (round to nearest even), then fp32 -> bf16 (round to nearest
+// even) on the bits.  Written as two conversions, the compiler folds them
+// into one rounding straight from fp64 (fp32 rounded to odd, then to bf16),
+// which differs wherever the fp32 value lands on a bf16 midpoint.
 __device__ __forceinline__ uint16_t f64_to_bf16(double x) {
-  return __builtin_bit_cast(uint16_t, static_cast<__bf16>((float)x));
-}
-
-// theta_j = base^(-2j/d), as (-2j)/d in double.
-__device__ __forceinline__ double inv_freq(int j, int d, double base) {
-  return pow(base, (-2.0 * (double)j) / (double)d);
+  const uint32_t u = __builtin_bit_cast(uint32_t, (float)x);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
 }
 
 // bf16 element i of a 16-byte piece
@@ -146,7 +146,7 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   constexpr int RW = 4;
   const int pieces = RE / 8;
   const int fj = lane % hd;
-  const double invf = inv_freq(fj, d, a.theta);
+  const double invf = a.inv_freq[fj];
   const int pm = d / 16;
   const int f0 = 8 * (lane % pm);
   const bool second = (lane & pm) != 0;
@@ -312,7 +312,7 @@ __global__ __launch_bounds__(RT) void reindex_decide3(DecideArgs a) {
 }
 
 // Distinct-rank compaction of one axis of one layer's retained coordinates.
-constexpr int kSpanWords = HERMES_MROPE_MAX_SPAN / 32;
+constexpr int kSpanWords = kMropeWindow / 32;
 __global__ __launch_bounds__(RT) void mrope_rank(RankArgs a) {
   const int jj = blockIdx.x, axis = blockIdx.y;
   const bool rot = a.reindex == 1 || (a.reindex == 2 && a.flag[0] != 0);
@@ -332,6 +332,7 @@ __global__ __launch_bounds__(RT) void mrope_rank(RankArgs a) {
   __shared__ uint32_t bits[kSpanWords];
   __shared__ uint32_t wpre[kSpanWords];
   __shared__ int red[2][RT / 64];
+  __shared__ long long rnext[RT / 64];
   __shared__ uint32_t wsum[RT / 64];
   // min and max of the retained coordinates
   int mn = INT_MAX, mx = INT_MIN;
@@ -354,50 +355,80 @@ __global__ __launch_bounds__(RT) void mrope_rank(RankArgs a) {
     mn = min(mn, red[0][w]);
     mx = max(mx, red[1][w]);
   }
-  const long long span = (long long)mx - (long long)mn + 1;
-  if (span > HERMES_MROPE_MAX_SPAN) {   // wider than the bitmap: coordinates kept
-    for (int r = tid; r < rows; r += RT) out[r] = coord(r);
-    return;
-  }
-  const int nwords = (int)((span + 31) / 32);
-  for (int w = tid; w < nwords; w += RT) bits[w] = 0u;
-  __syncthreads();
-  for (int r = tid; r < rows; r += RT) {
-    const int c = coord(r) - mn;
-    atomicOr(&bits[c >> 5], 1u << (c & 31));
-  }
-  __syncthreads();
-  // exclusive prefix of the word popcounts: thread t owns words [8t, 8t + 8)
-  constexpr int WPT = kSpanWords / RT;
-  uint32_t own = 0;
-#pragma unroll
-  for (int u = 0; u < WPT; ++u) {
-    const int w = tid * WPT + u;
-    own += w < nwords ? (uint32_t)__popc(bits[w]) : 0u;
-  }
-  uint32_t inc = own;
-#pragma unroll
-  for (int o = 1; o < 64; o <<= 1) {
-    const uint32_t x = __shfl_up(inc, o);
-    if (lane >= o) inc += x;
-  }
-  if (lane == 63) wsum[wv] = inc;
-  __syncthreads();
-  uint32_t base = inc - own;
-  for (int w = 0; w < wv; ++w) base += wsum[w];
-#pragma unroll
-  for (int u = 0; u < WPT; ++u) {
-    const int w = tid * WPT + u;
-    if (w < nwords) {
-      wpre[w] = base;
-      base += (uint32_t)__popc(bits[w]);
+  // The ranks are counted window by window: each pass marks the retained
+  // coordinates in [lo, lo + span) in the LDS bitmap, ranks the rows whose
+  // coordinate falls there after the `below` distinct coordinates of the
+  // earlier windows, and moves lo to the smallest coordinate past the window
+  // (so empty stretches of a wide axis cost nothing).  Axes narrower than the
+  // bitmap take one pass.
+  constexpr long long kSpan = kMropeWindow;
+  long long lo = mn;
+  uint32_t below = 0;
+  for (;;) {
+    const long long hi_ex = lo + kSpan;   // window [lo, hi_ex)
+    const long long top = (long long)mx + 1 < hi_ex ? (long long)mx + 1 : hi_ex;
+    const int nwords = (int)((top - lo + 31) / 32);
+    for (int w = tid; w < nwords; w += RT) bits[w] = 0u;
+    __syncthreads();
+    for (int r = tid; r < rows; r += RT) {
+      const long long c = (long long)coord(r) - lo;
+      if (c >= 0 && c < top - lo) atomicOr(&bits[c >> 5], 1u << (c & 31));
     }
-  }
-  __syncthreads();
-  for (int r = tid; r < rows; r += RT) {
-    const int c = coord(r) - mn;
-    const int w = c >> 5, b = c & 31;
-    out[r] = a.offset + (int)(wpre[w] + (uint32_t)__popc(bits[w] & ((1u << b) - 1u)));
+    __syncthreads();
+    // exclusive prefix of the word popcounts: thread t owns words [8t, 8t + 8)
+    constexpr int WPT = kSpanWords / RT;
+    uint32_t own = 0;
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int w = tid * WPT + u;
+      own += w < nwords ? (uint32_t)__popc(bits[w]) : 0u;
+    }
+    uint32_t inc = own;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const uint32_t x = __shfl_up(inc, o);
+      if (lane >= o) inc += x;
+    }
+    if (lane == 63) wsum[wv] = inc;
+    __syncthreads();
+    uint32_t base = inc - own, total = 0;
+    for (int w = 0; w < RT / 64; ++w) {
+      base += w < wv ? wsum[w] : 0u;
+      total += wsum[w];
+    }
+#pragma unroll
+    for (int u = 0; u < WPT; ++u) {
+      const int w = tid * WPT + u;
+      if (w < nwords) {
+        wpre[w] = base;
+        base += (uint32_t)__popc(bits[w]);
+      }
+    }
+    __syncthreads();
+    // ranks of this window's rows, and the first coordinate past it
+    long long nxt = LLONG_MAX;
+    for (int r = tid; r < rows; r += RT) {
+      const int cr = coord(r);
+      const long long c = (long long)cr - lo;
+      if (c >= 0 && c < top - lo) {
+        const int w = (int)(c >> 5), b = (int)(c & 31);
+        out[r] = a.offset + (int)(below + wpre[w] + (uint32_t)__popc(bits[w] & ((1u << b) - 1u)));
+      } else if (c >= top - lo) {
+        nxt = min(nxt, (long long)cr);
+      }
+    }
+#pragma unroll
+    for (int o = 32; o > 0; o >>= 1) {
+      const long long x = __shfl_xor(nxt, o);
+      nxt = x < nxt ? x : nxt;
+    }
+    if (lane == 0) rnext[wv] = nxt;
+    __syncthreads();
+    for (int w = 0; w < RT / 64; ++w) nxt = rnext[w] < nxt ? rnext[w] : nxt;
+    below += total;
+    if (nxt == LLONG_MAX) break;   // uniform: every thread read the same rnext
+    lo = nxt;
+    __syncthreads();   // rnext, bits and wpre are rewritten by the next pass
   }
 }
 
@@ -433,7 +464,7 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
   // 8 frequencies from 8 (c % (d/16)) on, and the other half of each of its
   // pairs sits in piece c ^ (d/16), held by lane lane ^ (d/16).
   const int fj = lane % hd;
-  const double invf = inv_freq(fj, d, a.theta);
+  const double invf = a.inv_freq[fj];
   const int pm = d / 16;
   const int f0 = 8 * (lane % pm);
   const bool second = (lane & pm) != 0;

@@ -189,6 +189,12 @@ void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
   }
 }
 
+// RoPE frequencies theta_j = base^(-2j/d), j < d/2 (rotate-half pairs), in
+// double on the host: the kernels read them instead of evaluating pow.
+void rope_frequencies(double base, int d, double *out) {
+  for (int j = 0; j < d / 2 && j < kMaxHalfDim; ++j) out[j] = std::pow(base, (-2.0 * (double)j) / (double)d);
+}
+
 // 10% shallow, 60% middle, 30% deep (Sec. 4.1), rounded to nearest layer.
 std::vector<int8_t> default_classes(int L) {
   const int n_sh = (int)std::floor(0.1 * L + 0.5);
@@ -898,7 +904,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
       sm.row_elems = ga.row_elems;
       sm.head_dim = ctx->D;
       sm.n_list = n_sum;
-      sm.theta = ctx->rope_theta;
+      rope_frequencies(ctx->rope_theta, ctx->D, sm.inv_freq);
       rc = ctx->run(HERMES_K_SUMMARY, s, [&] { return launch_summary(sm, max_T_sum, s); });
       if (rc != HERMES_OK) return rc;
     }
@@ -918,7 +924,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
     ga.reindex = ctx->reindex_mode == HERMES_REINDEX_EAGER ? 1
                : ctx->reindex_mode == HERMES_REINDEX_LAZY ? 2 : 0;
     ga.rope_offset = ctx->rope_offset;
-    ga.theta = ctx->rope_theta;
+    rope_frequencies(ctx->rope_theta, ctx->D, ga.inv_freq);
     ga.flag = flag;
     ga.sum_k = reinterpret_cast<const uint16_t *>(ctx->ws + ctx->lay.sumk);
     ga.sum_v = reinterpret_cast<const uint16_t *>(ctx->ws + ctx->lay.sumv);

@@ -10,6 +10,10 @@
 namespace hermes {
 
 constexpr int kMaxLayers = HERMES_MAX_LAYERS;
+constexpr int kMaxHalfDim = 64;   // frequency pairs of the largest head size (128)
+// 3D re-indexing ranks an axis's coordinates through an LDS bitmap over a
+// window of this many consecutive values, one window after another.
+constexpr int kMropeWindow = 262144;
 
 // Static per-layer description, uploaded once into the workspace.
 struct LayerTable {
@@ -114,7 +118,7 @@ struct GatherArgs {
   int32_t n_list;
   int32_t reindex;          // 0 never, 1 always, 2 when *flag != 0
   int32_t rope_offset;
-  double theta;             // RoPE base
+  double inv_freq[kMaxHalfDim];   // RoPE frequencies theta_j = base^(-2j/d), host-computed
   const int32_t *flag;      // lazy re-indexing decision (device)
   const uint16_t *sum_k, *sum_v;   // [n_layers][row_elems] staged summary rows
   const int32_t *sum_meta;  // [n_layers][4]: insert index, stream pos, RoPE pos, evicted
@@ -140,7 +144,7 @@ struct SummaryArgs {
   uint16_t *sum_k, *sum_v;  // [n_layers][row_elems]
   int32_t *sum_meta;        // [n_layers][4]
   int32_t row_elems, head_dim, n_list;
-  double theta;             // RoPE base
+  double inv_freq[kMaxHalfDim];   // RoPE frequencies theta_j = base^(-2j/d), host-computed
   int32_t len[kMaxLayers];      // by entry: candidates T
   int32_t budget[kMaxLayers];   // by entry: kept M
   int8_t layer_id[kMaxLayers];

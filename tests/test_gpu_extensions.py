@@ -6,10 +6,13 @@ Kept sets follow the core contract (bit-exact outside the 1e-6 band of the
 budget-th key).  The compacted cache is then rebuilt by the oracle from the
 GPU's own kept set, so near-tie swaps cannot leak into the comparison of the
 summary rows and the rotated keys.  Those are computed in fp64 on both sides
-and stored as bf16 through fp32; the two fp64 values differ only at the 1e-16
-level (pow, sincos, fused multiply-adds, summation order), which changes the
-stored bf16 only when the value sits at a rounding tie.  The bar: every
-element within one bf16 ulp and at most 1e-4 of the elements off by one."""
+and stored as bf16 through fp32 (two roundings to nearest even, also on the
+device, where the compiler would otherwise fold them into one); the RoPE
+frequencies come from the host's pow on both sides, so the two fp64 values
+differ only where the device's sincos or summation order differs from the
+host's at the 1e-16 level, which changes the stored bf16 only for a value
+within about 1e-16 of a rounding boundary.  The bar: every element within
+one bf16 ulp and at most 1e-6 of the elements off by one."""
 from __future__ import annotations
 
 import numpy as np
@@ -60,7 +63,7 @@ def _cmp_layer(l, kv, exp: he.ExtLayerCache, what):
             ulp = 2.0 ** (np.floor(np.log2(np.maximum(np.abs(e), 1e-30))) - 7)
             worst = float(np.max(np.abs(g - e)[diff] / ulp[diff]))
             say(f"{what} layer {l} {name}: {int(diff.sum())} of {diff.size} differ, worst {worst} ulp")
-            assert worst <= 1.0 and diff.mean() <= 1e-4, f"{what} layer {l}: {name} differs"
+            assert worst <= 1.0 and diff.mean() <= 1e-6, f"{what} layer {l}: {name} differs"
 
 
 def _run(wl, classes, ext: he.ExtConfig, caches, chunks, prompts=None, prompts_stacked=False,
@@ -357,27 +360,26 @@ def _grid(n, H, W, offset, t_step):
     return np.stack([offset + f * t_step, offset + r // W, offset + r % W], 1).astype(np.int64)
 
 
-@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128), (32, 8, 128)])
-@pytest.mark.parametrize("mode", ["eager", "lazy_fires", "lazy_waits"])
-def test_mrope_reindex(shape, mode):
-    """5 cached frames of 14 x 14 tokens (t step 2, text prefix 3) + 1 new
-    frame; the last layer keeps everything and is re-indexed in place."""
+def _mrope_case(shape, mode, section_gpu, section_oracle, t_step=2, frames=5):
+    """`frames` cached frames of 14 x 14 tokens (text prefix 3) + 1 new frame;
+    the last layer keeps everything and is re-indexed in place."""
     Hq, Hkv, d = shape
     classes = [S, M, D, D]
-    T0, C = 5 * 196, 196
-    wl = _wl("ext_mrope", 60 + d, 4, Hq, Hkv, d, T0, C, (500, 600, 700, 1200))
+    T0, C = frames * 196, 196
+    wl = _wl("ext_mrope", (60 if t_step == 2 else 160) + d, 4, Hq, Hkv, d, T0, C,
+             (500, 600, 700, T0 + C + 24))
     caches = [wk.gen_cache(wl, l) for l in range(4)]
     chunks = [wk.gen_chunk(wl, 0, l) for l in range(4)]
-    g = _grid(T0 + C, 14, 14, offset=3, t_step=2)
+    g = _grid(T0 + C, 14, 14, offset=3, t_step=t_step)
     for c in caches:
         c["thw"] = g[:T0].T.copy()
-    section = (8, 12, 12) if d == 64 else (16, 24, 24)
-    # the largest coordinate retained anywhere is h = w = 3 + 13 = 16 (t reaches 13)
+    # the largest coordinate retained anywhere is h = w = 3 + 13 = 16 (with
+    # t step 2, t reaches 13)
     limit = {"eager": 0, "lazy_fires": 18, "lazy_waits": 19}[mode]
     ext = he.ExtConfig(reindex_mode=he.REINDEX_EAGER if mode == "eager" else he.REINDEX_LAZY,
                        rope_offset=5, rope_limit=limit, rope_headroom=2, rope_axes=3,
-                       mrope_section=section)
-    say(f"mrope {shape} {mode}")
+                       mrope_section=section_oracle)
+    say(f"mrope {shape} {mode} section {section_gpu} t step {t_step}")
     ext_caches = [he.ExtLayerCache(f64(c["k"]), f64(c["v"]), c["pos"].astype(np.int64),
                                    g[:T0, 0].copy(), g[:T0].copy()) for c in caches]
     ext_chunks = [dict(ch, rope_thw=g[T0:].T.copy()) for ch in _ext_chunks(chunks)]
@@ -386,7 +388,7 @@ def test_mrope_reindex(shape, mode):
     assert ref["reindexed"] == (mode != "lazy_waits")
     kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, layer_class=classes,
                               reindex_mode=ext.reindex_mode, rope_offset=5, rope_limit=limit,
-                              rope_headroom=2, rope_axes=3, mrope_section=section)
+                              rope_headroom=2, rope_axes=3, mrope_section=section_gpu)
     t = streaming.chunk_tensors(_stack(chunks), "cuda")
     thw = torch.from_numpy(np.ascontiguousarray(g[T0:].T, dtype=np.int32)).cuda()
     kv.append(t["q"], t["k"], t["v"], t["pos"], rope_thw=thw)
@@ -398,6 +400,31 @@ def test_mrope_reindex(shape, mode):
         got = kv.view_mrope(l).cpu().numpy().T
         assert np.array_equal(got, compact[l].rpos3), f"layer {l}: coordinates differ"
     kv.close()
+
+
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128), (32, 8, 128)])
+@pytest.mark.parametrize("mode", ["eager", "lazy_fires", "lazy_waits"])
+def test_mrope_reindex(shape, mode):
+    d = shape[2]
+    section = (8, 12, 12) if d == 64 else (16, 24, 24)
+    _mrope_case(shape, mode, section, section)
+
+
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128)])
+def test_mrope_reindex_default_section(shape):
+    """mrope_section (0, 0, 0) selects the library's default split, which
+    must be the oracle's default (16/24/24 at d = 128, 8/12/12 at d = 64);
+    the benchmark's 3D re-indexing leg runs with it."""
+    _mrope_case(shape, "eager", (0, 0, 0), ())
+
+
+@pytest.mark.parametrize("t_step", [70001, 300007])
+def test_mrope_reindex_wide_t_axis(t_step):
+    """Temporal coordinates far apart (6 frames, t step 70001 or 300007: the
+    retained t values span more than one rank window of 2^18 values, with
+    empty stretches between frames): every axis is still ranked over all its
+    distinct retained coordinates (the appendix's sorted sets have no bound)."""
+    _mrope_case((28, 4, 128), "eager", (16, 24, 24), (16, 24, 24), t_step=t_step)
 
 
 def test_mrope_append_entry_points_follow_the_context():
