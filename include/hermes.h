@@ -181,6 +181,29 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
                    void *workspace, size_t ws_bytes, hermes_ctx **out);
 
 /*
+ * hermes_kv_init for callers that cannot allocate device memory (code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc):
+ * the workspace is the library's own device scratch, a file-scope array of
+ * HERMES_STATIC_WORKSPACE_BYTES that every GPU the library runs on holds
+ * until the process ends.  Nothing is allocated (no hipMalloc, no library
+ * routine that allocates); the scratch of the current device is looked up
+ * once per device and is owned by the returned context until
+ * hermes_kv_destroy.  The caller still owns the layer buffers, inputs and
+ * outputs.  One such context per device at a time: a second call on the same
+ * device returns HERMES_ESTATE while the first is alive, since both would
+ * share (and race on) the one array; nothing in it needs to start at zero
+ * (every word is written before it is read).  When the configuration's
+ * workspace (hermes_workspace_bytes) exceeds the scratch, the key-slice
+ * partial state of queries and guidance prompts is cut to what fits (queries
+ * then take fewer or no key slices: same results up to rounding order);
+ * HERMES_ECAPACITY when even the rest exceeds it.  Errors otherwise as
+ * hermes_kv_init (ENOTSUP also beyond 64 devices).
+ */
+enum { HERMES_STATIC_WORKSPACE_BYTES = 64 << 20 };
+int hermes_kv_init_static(const hermes_config *cfg, const hermes_layer_buffers *layers,
+                          hermes_ctx **out);
+
+/*
  * Chunk-wise prefill of one layer or of all layers (Sec. 2 setup, Sec. 4.1):
  * append n_new tokens (q, k, v device bf16; pos device int32 [n_new]) to the
  * cache, and write the attention output `out` (device bf16) of the chunk's

@@ -18,7 +18,8 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libhermes.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["attention.hip", "select.hip", "gather.hip", "extend.hip", "check.hip", "hermes_api.cpp"]
+SOURCES = ["attention.hip", "select.hip", "gather.hip", "extend.hip", "check.hip", "scratch.hip",
+           "hermes_api.cpp"]
 COMMON = ["-O3", "-std=c++17", "-fPIC", "--offload-arch=gfx950", f"-I{INCLUDE}", f"-I{CSRC}",
           "-Wall", "-Wno-unused-result"]
 # Packed-FP32 VALU forms stay off: the compiler would otherwise emit them

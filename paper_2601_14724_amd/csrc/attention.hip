@@ -365,7 +365,10 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   if constexpr (SPLIT) {
     // unnormalised partial state of this key slice
     if (row_ok) {
-      const int64_t row = ((int64_t)(j * Hkv + kv) * kMaxSplits + split) * a.part_rows + prow;
+      // partial block of (entry j, KV head kv, slice split): entry j's blocks
+      // start after the Hkv * nsp blocks of every earlier entry
+      const int64_t blk = a.wg_start[j] / nqt + (int64_t)kv * nsp + split;
+      const int64_t row = blk * a.part_rows + prow;
       // bf16 halves the state the combine reads back; the maximum and the
       // row sum, which fix the LSE, stay fp32
       uint16_t *op = a.opart + row * D;
@@ -417,7 +420,8 @@ __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= P * (D / 8)) return;
   const int p = e / (D / 8), c8 = e % (D / 8);
-  const int64_t row0 = (int64_t)(j * a.Hkv + kv) * kMaxSplits * a.part_rows + p;
+  const int nqt = (P + BM - 1) / BM;
+  const int64_t row0 = (a.wg_start[j] / nqt + (int64_t)kv * nsp) * a.part_rows + p;
   float m = -INFINITY;
   for (int s = 0; s < nsp; ++s) m = fmaxf(m, a.mlpart[2 * (row0 + (int64_t)s * a.part_rows)]);
   float lsum = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};

@@ -28,6 +28,7 @@ struct Layout {
   int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride, normpart_lstride,
       newc_lstride;
   int32_t part_rows;
+  int64_t part_blocks;      // key-slice partial blocks of part_rows rows the workspace holds
 };
 
 int max_budget(const hermes_config *c) {
@@ -81,7 +82,10 @@ int check_config(const hermes_config *c) {
   return HERMES_OK;
 }
 
-Layout layout_of(const hermes_config *c) {
+// Workspace layout of `c`; part_blocks < 0 sizes the key-slice partial state
+// for the most slices any query can take (every layer and KV head cut into
+// kMaxSplits slices), else for that many partial blocks.
+Layout layout_of(const hermes_config *c, int64_t part_blocks = -1) {
   Layout s;
   s.lse_lstride = (int64_t)c->n_q_heads * c->max_chunk;
   s.keys_lstride = c->max_cap;
@@ -122,13 +126,34 @@ Layout layout_of(const hermes_config *c) {
   off = round_up(off + sizeof(int32_t) * 4);
   // split-key partial state of short passes (query, guidance prompt)
   s.part_rows = kSplitMaxTokens * (c->n_q_heads / c->n_kv_heads);
-  const size_t prow = (size_t)c->n_layers * c->n_kv_heads * kMaxSplits * s.part_rows;
+  s.part_blocks = part_blocks >= 0 ? part_blocks : (int64_t)c->n_layers * c->n_kv_heads * kMaxSplits;
+  const size_t prow = (size_t)s.part_blocks * s.part_rows;
   s.opart = off;
   off = round_up(off + sizeof(uint16_t) * prow * c->head_dim);
   s.mlpart = off;
   off = round_up(off + sizeof(float) * prow * 2);
   s.total = off;
   return s;
+}
+
+// The layout of `c` in at most `limit` bytes: the default one if it fits,
+// else the same with as many key-slice partial blocks as the rest leaves
+// (possibly none: queries then run unsliced).  false if even that exceeds
+// `limit`.
+bool layout_within(const hermes_config *c, size_t limit, Layout *out) {
+  const Layout full = layout_of(c);
+  if (full.total <= limit) {
+    *out = full;
+    return true;
+  }
+  const Layout none = layout_of(c, 0);
+  if (none.total > limit) return false;
+  const size_t per_block = (size_t)none.part_rows * (sizeof(uint16_t) * c->head_dim + 2 * sizeof(float));
+  int64_t blocks = (int64_t)((limit - none.total) / per_block);
+  // the two regions are rounded up separately: back off until it fits
+  while (blocks > 0 && layout_of(c, blocks).total > limit) --blocks;
+  *out = layout_of(c, blocks);
+  return true;
 }
 
 // Key slices of a short pass (n_rows <= kSplitMaxTokens rows per entry over
@@ -141,7 +166,7 @@ Layout layout_of(const hermes_config *c) {
 // (entry, KV head, query tile) runs over its whole cache, so the entry with
 // the longest cache sets the time while the others' CUs idle.  Fills nsp,
 // wg_start and nsplit (the largest nsp; 1 means the plain kernel).
-void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
+void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D, int64_t max_blocks) {
   const int nqt = (n_rows * G + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
   std::vector<int> tiles(n_list);
   int max_tiles = 1;
@@ -171,6 +196,12 @@ void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D) {
         longest = len > longest ? len : longest;
       }
       if (most == 1) continue;
+      int64_t blocks = 0;   // partial blocks: one per (entry, KV head, slice)
+      for (int j = 0; j < n_list; ++j) {
+        const int ns = (tiles[j] + m - 1) / m;
+        blocks += (int64_t)Hkv * (ns < kMaxSplits ? ns : kMaxSplits);
+      }
+      if (blocks > max_blocks) continue;
       const double cost = rounds(w) * (longest + 2.0) + 2.0 + (double)w * D / (64.0 * 128.0);
       if (cost < best) {
         best = cost;
@@ -239,6 +270,7 @@ struct hermes_ctx {
   LayerTable *d_tab = nullptr;
   bool prof = false;
   bool check = false;   // device-side precondition checks before each call's launches
+  int static_dev = -1;  // device whose static scratch is the workspace (-1: the caller's)
   std::vector<EventPair> used[HERMES_K_COUNT];
   std::vector<EventPair> pool;
 
@@ -336,15 +368,12 @@ size_t hermes_workspace_bytes(const hermes_config *cfg) {
   return layout_of(cfg).total;
 }
 
-int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers, void *workspace,
-                   size_t ws_bytes, hermes_ctx **out) {
-  if (out == nullptr) return HERMES_EINVAL;
-  *out = nullptr;
-  const int rc = check_config(cfg);
-  if (rc != HERMES_OK) return rc;
-  if (layers == nullptr || workspace == nullptr || !aligned(workspace, kAlign)) return HERMES_EINVAL;
-  const Layout lay = layout_of(cfg);
-  if (ws_bytes < lay.total) return HERMES_ECAPACITY;
+}  // extern "C"
+
+// Buffer checks and context creation over a workspace of layout `lay`.
+static int init_context(const hermes_config *cfg, const hermes_layer_buffers *layers, void *workspace,
+                        const Layout &lay, hermes_ctx **out) {
+  if (layers == nullptr) return HERMES_EINVAL;
   const int L = cfg->n_layers;
   for (int l = 0; l < L; ++l) {
     const hermes_layer_buffers &b = layers[l];
@@ -475,8 +504,45 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
   return HERMES_OK;
 }
 
+extern "C" {
+
+int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers, void *workspace,
+                   size_t ws_bytes, hermes_ctx **out) {
+  if (out == nullptr) return HERMES_EINVAL;
+  *out = nullptr;
+  const int rc = check_config(cfg);
+  if (rc != HERMES_OK) return rc;
+  if (layers == nullptr || workspace == nullptr || !aligned(workspace, kAlign)) return HERMES_EINVAL;
+  const Layout lay = layout_of(cfg);
+  if (ws_bytes < lay.total) return HERMES_ECAPACITY;
+  return init_context(cfg, layers, workspace, lay, out);
+}
+
+int hermes_kv_init_static(const hermes_config *cfg, const hermes_layer_buffers *layers,
+                          hermes_ctx **out) {
+  if (out == nullptr) return HERMES_EINVAL;
+  *out = nullptr;
+  int rc = check_config(cfg);
+  if (rc != HERMES_OK) return rc;
+  if (layers == nullptr) return HERMES_EINVAL;
+  Layout lay;
+  if (!layout_within(cfg, kStaticWorkspaceBytes, &lay)) return HERMES_ECAPACITY;
+  void *ws = nullptr;
+  int dev = -1;
+  rc = static_workspace_acquire(&ws, &dev);
+  if (rc != HERMES_OK) return rc;
+  rc = init_context(cfg, layers, ws, lay, out);
+  if (rc != HERMES_OK) {
+    static_workspace_release(dev);
+    return rc;
+  }
+  (*out)->static_dev = dev;
+  return HERMES_OK;
+}
+
 void hermes_kv_destroy(hermes_ctx *ctx) {
   if (ctx == nullptr) return;
+  if (ctx->static_dev >= 0) static_workspace_release(ctx->static_dev);
   for (auto &v : ctx->used)
     for (auto &e : v) {
       (void)hipEventDestroy(e.start);
@@ -792,7 +858,7 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
     max_T = ctx->len[l] > max_T ? ctx->len[l] : max_T;
   }
   const int n = (int)list.size();
-  split_plan(at, n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D);
+  split_plan(at, n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D, ctx->lay.part_blocks);
   at.part_rows = ctx->lay.part_rows;
   at.opart = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
@@ -1035,7 +1101,7 @@ int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const voi
     at.cur[n] = ctx->cur[l];
     ++n;
   }
-  split_plan(at, n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D);
+  split_plan(at, n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D, ctx->lay.part_blocks);
   at.part_rows = ctx->lay.part_rows;
   at.opart = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);

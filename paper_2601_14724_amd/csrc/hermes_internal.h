@@ -53,8 +53,9 @@ struct AttnArgs {
   // Split-key mode (short passes): entry j's key tiles are cut into nsp[j]
   // slices (at most kMaxSplits; nsplit is the largest), workgroups
   // [wg_start[j], wg_start[j+1]) cover entry j, and each writes unnormalised
-  // O (bf16), the running maximum and the row sum (fp32) of its slice to opart / mlpart
-  // [entry][Hkv][kMaxSplits][part_rows]; a combine kernel merges the slices.
+  // O (bf16), the running maximum and the row sum (fp32) of its slice to
+  // opart / mlpart [block][part_rows], block = (Hkv * nsp of the earlier
+  // entries) + kv * nsp[j] + slice; a combine kernel merges the slices.
   int32_t nsplit, part_rows;
   int8_t nsp[kMaxLayers];
   int32_t wg_start[kMaxLayers + 1];
@@ -203,6 +204,15 @@ struct AppendArgs {
   int8_t slot[kMaxLayers];
   int8_t cur[kMaxLayers];
 };
+
+// Device scratch of the no-allocation context entry point (scratch.hip):
+// kStaticWorkspaceBytes per GPU.  acquire looks up the array's address on the
+// current device (once per device) and marks it owned: HERMES_ESTATE while
+// another context owns it, HERMES_ENOTSUP beyond kMaxDevices GPUs.
+constexpr size_t kStaticWorkspaceBytes = (size_t)HERMES_STATIC_WORKSPACE_BYTES;
+constexpr int kMaxDevices = 64;
+int static_workspace_acquire(void **ptr, int *device);
+void static_workspace_release(int device);
 
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);

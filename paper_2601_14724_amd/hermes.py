@@ -35,7 +35,8 @@ EXPORTED = ("hermes_workspace_bytes", "hermes_kv_init", "hermes_append_chunk",
             "hermes_kv_view", "hermes_kv_view_rope", "hermes_kv_view_mrope",
             "hermes_budget_from_weights", "hermes_kv_destroy", "hermes_strerror",
             "hermes_select_topk", "hermes_profile_enable", "hermes_profile_read",
-            "hermes_check_enable")
+            "hermes_check_enable", "hermes_kv_init_static")
+STATIC_WORKSPACE_BYTES = 64 << 20
 
 
 class HermesConfig(ctypes.Structure):
@@ -71,6 +72,9 @@ lib.hermes_workspace_bytes.argtypes = [ctypes.POINTER(HermesConfig)]
 lib.hermes_kv_init.restype = ctypes.c_int
 lib.hermes_kv_init.argtypes = [ctypes.POINTER(HermesConfig), ctypes.POINTER(LayerBuffers), _vp,
                                ctypes.c_size_t, ctypes.POINTER(_vp)]
+lib.hermes_kv_init_static.restype = ctypes.c_int
+lib.hermes_kv_init_static.argtypes = [ctypes.POINTER(HermesConfig), ctypes.POINTER(LayerBuffers),
+                                      ctypes.POINTER(_vp)]
 lib.hermes_append_chunk.restype = ctypes.c_int
 lib.hermes_append_chunk.argtypes = [_vp, _i32, _vp, _vp, _vp, _vp, _i32, _vp, _vp]
 lib.hermes_append_chunk_at.restype = ctypes.c_int
@@ -178,7 +182,7 @@ class HermesKV:
                  summary_mode: int = 0, reindex_mode: int = REINDEX_NONE, rope_offset: int = 0,
                  rope_limit: int = 0, rope_headroom: int = 0, rope_theta: float = 1.0e6,
                  scoring_mode: int = SCORE_CHUNK, rope_axes: int = 1,
-                 mrope_section: Sequence[int] = (0, 0, 0)):
+                 mrope_section: Sequence[int] = (0, 0, 0), static_workspace: bool = False):
         self.L, self.Hq, self.Hkv, self.d = n_layers, n_q_heads, n_kv_heads, head_dim
         self.budgets = [int(b) for b in budgets]
         self.max_chunk = int(max_chunk)
@@ -250,7 +254,9 @@ class HermesKV:
         nbytes = lib.hermes_workspace_bytes(ctypes.byref(cfg))
         if nbytes == 0:
             raise HermesError(EINVAL, "hermes_workspace_bytes")
-        self.workspace = torch.empty(nbytes, dtype=torch.uint8, device=dev)
+        # static_workspace: the library's own device scratch (hermes_kv_init_static)
+        self.workspace = (None if static_workspace
+                          else torch.empty(nbytes, dtype=torch.uint8, device=dev))
         bufs = (LayerBuffers * n_layers)()
         for l in range(n_layers):
             b = bufs[l]
@@ -272,8 +278,13 @@ class HermesKV:
                     b.rpos_w[p] = self.rpos_w[l][p].data_ptr()
         self._bufs = bufs
         ctx = ctypes.c_void_p()
-        check(lib.hermes_kv_init(ctypes.byref(cfg), bufs, self.workspace.data_ptr(), nbytes,
-                                 ctypes.byref(ctx)), "hermes_kv_init")
+        if static_workspace:
+            with torch.cuda.device(dev):
+                check(lib.hermes_kv_init_static(ctypes.byref(cfg), bufs, ctypes.byref(ctx)),
+                      "hermes_kv_init_static")
+        else:
+            check(lib.hermes_kv_init(ctypes.byref(cfg), bufs, self.workspace.data_ptr(), nbytes,
+                                     ctypes.byref(ctx)), "hermes_kv_init")
         self.ctx = ctx
 
     # ------------------------------------------------------------------ calls

@@ -72,6 +72,20 @@ def _init(cfg, bufs, ws=FAKE, nbytes=None):
     return rc, ctx
 
 
+def test_static_init_rejects_workspaces_beyond_the_scratch():
+    """hermes_kv_init_static refuses a configuration whose workspace, even
+    without the key-slice partial state, exceeds the library's static device
+    scratch; the size check runs before any device call."""
+    cfg = _cfg(max_cap=1 << 22)
+    need = H.lib.hermes_workspace_bytes(ctypes.byref(cfg))
+    assert need > H.STATIC_WORKSPACE_BYTES
+    bufs = (H.LayerBuffers * cfg.n_layers)()
+    ctx = ctypes.c_void_p()
+    assert H.lib.hermes_kv_init_static(ctypes.byref(cfg), bufs, ctypes.byref(ctx)) == H.ECAPACITY
+    assert not ctx.value
+    assert H.lib.hermes_kv_init_static(None, bufs, ctypes.byref(ctx)) == H.EINVAL
+
+
 def test_workspace_bytes():
     good = H.lib.hermes_workspace_bytes(ctypes.byref(_cfg()))
     assert good > 0 and good % 256 == 0
