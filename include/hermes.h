@@ -115,7 +115,8 @@ typedef struct {
                               3: M-RoPE (t, h, w) coordinates, t in rpos and h, w
                               in rpos_h / rpos_w, chunks appended through
                               hermes_append_chunk_mrope (appendix, 3D M-RoPE
-                              re-indexing); needs summary_mode 0                 */
+                              re-indexing); with summary_mode 1 the summary
+                              takes the newest evicted token's (t, h, w)        */
   int32_t mrope_section[3];/* rope_axes 3: frequency pairs j = 0 .. head_dim/2 - 1
                               of the t, h and w sections, in that order (sum
                               head_dim/2); all 0 selects head_dim/8 pairs for t
@@ -274,9 +275,11 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
  * algorithm): each evicting deep layer folds its evicted tokens into one
  * token, V = mean of the evicted values, K = mean of the evicted keys each
  * rotated from its RoPE position to t, the RoPE position of the newest
- * evicted token.  The summary takes that token's stream and RoPE position
- * and its sorted place among the kept rows, in addition to the budget
- * (length budget + 1).  K and V are accumulated in fp64, stored as bf16.
+ * evicted token (with rope_axes 3: each frequency pair turned by the change
+ * of its section's coordinate to the newest evicted token's (t, h, w)).
+ * The summary takes that token's stream and RoPE position (coordinates) and
+ * its sorted place among the kept rows, in addition to the budget (length
+ * budget + 1).  K and V are accumulated in fp64, stored as bf16.
  *
  * reindex_mode (Sec. 3.3; appendix 1D re-indexing): EAGER re-indexes every
  * layer at every call, LAZY only when the largest retained RoPE position of

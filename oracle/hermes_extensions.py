@@ -51,7 +51,12 @@ Readings where the paper is silent (each listed in the design notes):
     and the rest halved between h and w: 16/24/24 at d = 128, the backbone's
     split); the rank on an axis counts DISTINCT retained coordinates, so
     tokens that shared a coordinate still share it; the same offset applies
-    to every axis; summary tokens are not combined with 3D coordinates;
+    to every axis;
+  * summary tokens with 3D coordinates: the target is the newest evicted
+    token's (t, h, w), each evicted key is aligned to it section by section
+    (pair j turns by the change of the coordinate of its section), and the
+    summary takes that token's stream position and coordinates, inserted at
+    its sorted place as in 1D;
   * guidance rows attend every token of the cache and their own earlier rows
     (the prompt follows the video); only the cached tokens are candidates and
     every one of them is seen by all prompt rows, so alpha_mode 0 divides by
@@ -173,6 +178,20 @@ def rotary_delta3(k: np.ndarray, delta3: np.ndarray, section,
     s = np.sin(ang)[:, None, :]
     re, im = k[..., :half], k[..., half:]
     return np.concatenate([re * c - im * s, im * c + re * s], axis=-1)
+
+
+def summary_token3(k_ev: np.ndarray, v_ev: np.ndarray, coords_ev: np.ndarray, section,
+                   theta: float = DEFAULT_ROPE_THETA):
+    """The summary-token algorithm with 3D coordinates: v_sum = Mean(V_p);
+    every pruned key is aligned to the target (t, h, w) of the newest pruned
+    token (the last in stream order) by the sectioned RotaryDelta, then
+    k_sum = Mean(K_aligned).  Returns (k_sum [H][d], v_sum [H][d], target
+    [3]) in fp64, before storage rounding."""
+    coords_ev = np.asarray(coords_ev, dtype=np.int64)
+    target = coords_ev[-1].copy()
+    v_sum = v_ev.mean(axis=0)
+    aligned = rotary_delta3(k_ev, target[None, :] - coords_ev, section, theta)
+    return aligned.mean(axis=0), v_sum, target
 
 
 def reindex_coords3(coords: np.ndarray, offset: int) -> np.ndarray:
@@ -338,24 +357,32 @@ def compact_layer(cat: ExtLayerCache, idx: np.ndarray, deep: bool, ext: ExtConfi
     evicted rows at the sorted place of the newest evicted token."""
     T = cat.k.shape[0]
     k, v, pos, rpos = cat.k[idx], cat.v[idx], cat.pos[idx], cat.rpos[idx]
-    if ext.rope_axes == 3:
-        assert not ext.summary, "summary tokens are not combined with 3D coordinates"
-        return ExtLayerCache(k, v, pos, rpos, cat.rpos3[idx]), None
+    three = ext.rope_axes == 3
+    rpos3 = cat.rpos3[idx] if three else None
     summ = None
     if ext.summary and deep and len(idx) < T:
         mask = np.ones(T, dtype=bool)
         mask[idx] = False
         ev = np.nonzero(mask)[0]
-        ks, vs, t = summary_token(cat.k[ev], cat.v[ev], cat.rpos[ev], ext.rope_theta)
+        if three:
+            section = ext.mrope_section or default_mrope_section(cat.k.shape[-1])
+            ks, vs, tgt = summary_token3(cat.k[ev], cat.v[ev], cat.rpos3[ev], section, ext.rope_theta)
+            t = int(tgt[0])
+        else:
+            ks, vs, t = summary_token(cat.k[ev], cat.v[ev], cat.rpos[ev], ext.rope_theta)
         newest = int(ev[-1])
         ins = int(np.searchsorted(idx, newest))
         k = np.insert(k, ins, round_to_bf16(ks), axis=0)
         v = np.insert(v, ins, round_to_bf16(vs), axis=0)
         pos = np.insert(pos, ins, cat.pos[newest])
         rpos = np.insert(rpos, ins, t)
+        if three:
+            rpos3 = np.insert(rpos3, ins, tgt, axis=0)
         summ = {"index": ins, "source": newest, "t": t, "evicted": ev,
                 "k": round_to_bf16(ks), "v": round_to_bf16(vs)}
-    return ExtLayerCache(k, v, pos, rpos), summ
+        if three:
+            summ["target"] = tgt
+    return ExtLayerCache(k, v, pos, rpos, rpos3), summ
 
 
 def reindex_layers(compact: List[ExtLayerCache], ext: ExtConfig):

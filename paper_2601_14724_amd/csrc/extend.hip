@@ -113,7 +113,7 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   const uint16_t *V = L.v[cur];
   const int RE = a.row_elems, d = a.head_dim, hd = d / 2;
 
-  __shared__ int s_t, s_k0, s_k1;
+  __shared__ int s_t, s_h, s_w, s_k0, s_k1;
   __shared__ uint8_t is_kept[kSummaryRows];
   __shared__ double red[4][2 * 64 * 8 * PG];
   const int tid = threadIdx.x, wave = __builtin_amdgcn_readfirstlane(tid >> 6), lane = tid & 63;
@@ -124,7 +124,12 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   // a monotone predicate.
   if (wave == 0) {
     const int f = wave_search(M, [&](int j) { return kept[j] == T - M + j; });
-    if (lane == 0) s_t = rpos[T - M + f - 1];
+    if (lane == 0) {
+      const int newest = T - M + f - 1;
+      s_t = rpos[newest];
+      s_h = a.axes == 3 ? L.rpos_h[cur][newest] : 0;
+      s_w = a.axes == 3 ? L.rpos_w[cur][newest] : 0;
+    }
   } else if (wave == 1) {
     const int k0 = wave_search(M, [&](int j) { return kept[j] >= r0; });
     if (lane == 0) s_k0 = k0;
@@ -136,10 +141,11 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   __syncthreads();
   for (int i = s_k0 + tid; i < s_k1; i += NT) is_kept[kept[i] - r0] = 1;
   __syncthreads();
-  const int t = s_t;
+  const int t = s_t, th = s_h, tw = s_w;
 
   // Lane c sums the 16-byte pieces c and c + 64 of the evicted rows' K
-  // (turned to t) and V, in row order; the turn uses the pair partner from
+  // (turned to t; with M-RoPE each frequency pair by the change of its
+  // section's coordinate, to the target's (t, h, w)) and V, in row order; the turn uses the pair partner from
   // the lane whose piece index differs in bit d/16 and one fp64 sine/cosine
   // per lane and row (lane f evaluates frequency f % (d/2)), shared through
   // LDS.  Four rows are loaded before the first is summed.
@@ -150,6 +156,9 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
   const int pm = d / 16;
   const int f0 = 8 * (lane % pm);
   const bool second = (lane & pm) != 0;
+  const bool three = a.axes == 3;
+  const int my_axis = !three ? 0 : fj < a.section[0] ? 0 : fj < a.section[0] + a.section[1] ? 1 : 2;
+  const int32_t *rph = three ? L.rpos_h[cur] : nullptr, *rpw = three ? L.rpos_w[cur] : nullptr;
   __shared__ double2 trig[NT / 64][64];
   double ak[PG][8], av[PG][8];
 #pragma unroll
@@ -177,8 +186,9 @@ __global__ __launch_bounds__(NT) void summary_partial(SummaryArgs a) {
     for (int u = 0; u < RW; ++u) {
       if (!ev[u]) continue;   // uniform over the wave (one row)
       const int i = i0 + 4 * u;
+      const int delta = my_axis == 0 ? t - rpos[i] : my_axis == 1 ? th - rph[i] : tw - rpw[i];
       double sn, cs;
-      sincos((double)(t - rpos[i]) * invf, &sn, &cs);
+      sincos((double)delta * invf, &sn, &cs);
       trig[wave][lane] = double2{cs, sn};
       __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 #pragma unroll
@@ -247,11 +257,15 @@ __global__ __launch_bounds__(NT) void summary_finalize(SummaryArgs a) {
     const int f = wave_search(M, [&](int j) { return kept[j] == T - M + j; });
     if (threadIdx.x == 0) {
       const int newest = T - M + f - 1;
-      int32_t *meta = a.sum_meta + 4 * l;
+      int32_t *meta = a.sum_meta + kSumMeta * l;
       meta[0] = f;                       // kept entries before it
       meta[1] = L.pos[cur][newest];
       meta[2] = L.rpos[cur][newest];
       meta[3] = T - M;                   // tokens folded in
+      if (a.axes == 3) {
+        meta[4] = L.rpos_h[cur][newest];
+        meta[5] = L.rpos_w[cur][newest];
+      }
     }
   }
 }
@@ -268,7 +282,7 @@ __global__ __launch_bounds__(64) void reindex_decide(DecideArgs a) {
     const int32_t *rp = L.rpos[a.cur[l]];
     if (a.evicts[l]) {
       r = rp[a.kept[l * a.kept_lstride + a.budget[l] - 1]];
-      if (a.has_sum[l] && (long long)a.sum_meta[4 * l + 2] > r) r = a.sum_meta[4 * l + 2];
+      if (a.has_sum[l] && (long long)a.sum_meta[kSumMeta * l + 2] > r) r = a.sum_meta[kSumMeta * l + 2];
     } else if (a.len[l] > 0) {
       r = rp[a.len[l] - 1];
     }
@@ -294,6 +308,11 @@ __global__ __launch_bounds__(RT) void reindex_decide3(DecideArgs a) {
     for (int i = threadIdx.x; i < rows; i += RT) {
       const int src = a.evicts[l] ? min(max(kept[i], 0), L.cap - 1) : i;
       const long long m = max(L.rpos[c][src], max(L.rpos_h[c][src], L.rpos_w[c][src]));
+      r = m > r ? m : r;
+    }
+    if (a.evicts[l] && a.has_sum[l] && threadIdx.x == 0) {   // the summary's (t, h, w)
+      const int32_t *meta = a.sum_meta + kSumMeta * l;
+      const long long m = max(meta[2], max(meta[4], meta[5]));
       r = m > r ? m : r;
     }
   }
@@ -327,7 +346,17 @@ __global__ __launch_bounds__(RT) void mrope_rank(RankArgs a) {
   const int32_t *kept = a.kept + l * a.kept_lstride;
   int32_t *out = a.newc + (int64_t)(l * 3 + axis) * a.newc_lstride;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
-  auto coord = [&](int r) { return C[inplace ? r : min(max(kept[r], 0), L.cap - 1)]; };
+  // output row r of an evicting layer with a summary: kept rows before the
+  // summary's insert index, the summary, then the rest of the kept rows
+  const bool has_sum = !inplace && a.has_sum[jj] != 0;
+  const int32_t *meta = a.sum_meta + kSumMeta * l;
+  const int ins = has_sum ? meta[0] : -1;
+  const int sum_c = has_sum ? meta[axis == 0 ? 2 : axis == 1 ? 4 : 5] : 0;
+  auto coord = [&](int r) {
+    if (inplace) return C[r];
+    if (r == ins) return sum_c;
+    return C[min(max(kept[r - (has_sum && r > ins ? 1 : 0)], 0), L.cap - 1)];
+  };
 
   __shared__ uint32_t bits[kSpanWords];
   __shared__ uint32_t wpre[kSpanWords];
@@ -452,7 +481,7 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
   const bool rot = a.reindex == 1 || (a.reindex == 2 && a.flag[0] != 0);
   if ((inplace && !rot) || pieces > 64 * PG) return;
   const bool has_sum = a.has_sum[jj] != 0;
-  const int ins = has_sum ? a.sum_meta[4 * l] : -1;
+  const int ins = has_sum ? a.sum_meta[kSumMeta * l] : -1;
   const int32_t *kept = a.kept + l * a.kept_lstride;
   const uint16_t *Ks = L.k[cur], *Vs = L.v[cur];
   uint16_t *Kd = L.k[dst_buf], *Vd = L.v[dst_buf];
@@ -495,8 +524,8 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
         kr[u] = a.sum_k + (int64_t)l * RE;
         vr[u] = a.sum_v + (int64_t)l * RE;
         src[u] = -1;
-        p_src[u] = a.sum_meta[4 * l + 1];
-        r_src[u] = a.sum_meta[4 * l + 2];
+        p_src[u] = a.sum_meta[kSumMeta * l + 1];
+        r_src[u] = a.sum_meta[kSumMeta * l + 2];
       } else {
         src[u] = __builtin_amdgcn_readfirstlane(
             min(max(kept[j - (has_sum && j > ins ? 1 : 0)], 0), L.cap - 1));
@@ -506,9 +535,9 @@ __global__ __launch_bounds__(NT) void gather_rope(GatherArgs a) {
         r_src[u] = __builtin_amdgcn_readfirstlane(Rs[src[u]]);
       }
       h_old[u] = w_old[u] = c_new[u][0] = c_new[u][1] = c_new[u][2] = 0;
-      if (three) {   // no summary rows with M-RoPE: src >= 0
-        h_old[u] = __builtin_amdgcn_readfirstlane(Hs[src[u]]);
-        w_old[u] = __builtin_amdgcn_readfirstlane(Ws[src[u]]);
+      if (three) {   // the summary row carries the target's (t, h, w)
+        h_old[u] = src[u] < 0 ? a.sum_meta[kSumMeta * l + 4] : __builtin_amdgcn_readfirstlane(Hs[src[u]]);
+        w_old[u] = src[u] < 0 ? a.sum_meta[kSumMeta * l + 5] : __builtin_amdgcn_readfirstlane(Ws[src[u]]);
 #pragma unroll
         for (int x = 0; x < 3; ++x)
           c_new[u][x] = __builtin_amdgcn_readfirstlane(nc[x * a.newc_lstride + j]);

@@ -69,7 +69,6 @@ int check_config(const hermes_config *c) {
   if (!std::isfinite(c->rope_theta)) return HERMES_EINVAL;
   if (c->rope_axes != 0 && c->rope_axes != 1 && c->rope_axes != 3) return HERMES_EINVAL;
   if (c->rope_axes == 3) {
-    if (c->summary_mode) return HERMES_ENOTSUP;   // summary tokens carry one RoPE position
     const int *sec = c->mrope_section;
     if (sec[0] != 0 || sec[1] != 0 || sec[2] != 0) {
       if (sec[0] < 0 || sec[1] < 0 || sec[2] < 0) return HERMES_EINVAL;
@@ -121,7 +120,7 @@ Layout layout_of(const hermes_config *c, int64_t part_blocks = -1) {
   s.sumv = off;
   off = round_up(off + (c->summary_mode ? sizeof(uint16_t) * (size_t)row * c->n_layers : 0));
   s.smeta = off;
-  off = round_up(off + sizeof(int32_t) * 4 * (size_t)c->n_layers);
+  off = round_up(off + sizeof(int32_t) * kSumMeta * (size_t)c->n_layers);
   s.flag = off;
   off = round_up(off + sizeof(int32_t) * 4);
   // split-key partial state of short passes (query, guidance prompt)
@@ -970,6 +969,8 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
       sm.row_elems = ga.row_elems;
       sm.head_dim = ctx->D;
       sm.n_list = n_sum;
+      sm.axes = ctx->rope_axes;
+      for (int a = 0; a < 3; ++a) sm.section[a] = ctx->section[a];
       rope_frequencies(ctx->rope_theta, ctx->D, sm.inv_freq);
       rc = ctx->run(HERMES_K_SUMMARY, s, [&] { return launch_summary(sm, max_T_sum, s); });
       if (rc != HERMES_OK) return rc;
@@ -1029,6 +1030,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
       ra.kept_lstride = sa.kept_lstride;
       ra.newc = reinterpret_cast<int32_t *>(ctx->ws + ctx->lay.newc);
       ra.newc_lstride = ctx->lay.newc_lstride;
+      ra.sum_meta = meta;
       ra.flag = flag;
       ra.reindex = ga.reindex;
       ra.offset = ctx->rope_offset;
@@ -1037,6 +1039,7 @@ int hermes_compress(hermes_ctx *ctx, void *stream) {
         ra.layer_id[j] = ga.layer_id[j];
         ra.cur[j] = ga.cur[j];
         ra.mode[j] = ga.mode[j];
+        ra.has_sum[j] = ga.has_sum[j];
         ra.row_start[j + 1] = ga.row_start[j + 1];
       }
       rc = ctx->run(HERMES_K_GATHER, s, [&] { return launch_mrope_rank(ra, s); });

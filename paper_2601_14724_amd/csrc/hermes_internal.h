@@ -11,6 +11,9 @@ namespace hermes {
 
 constexpr int kMaxLayers = HERMES_MAX_LAYERS;
 constexpr int kMaxHalfDim = 64;   // frequency pairs of the largest head size (128)
+// Summary metadata per layer: insert index, stream position, RoPE position
+// (t with M-RoPE), evicted count, then h and w with M-RoPE.
+constexpr int kSumMeta = 8;
 // 3D re-indexing ranks an axis's coordinates through an LDS bitmap over a
 // window of this many consecutive values, one window after another.
 constexpr int kMropeWindow = 262144;
@@ -122,7 +125,7 @@ struct GatherArgs {
   double inv_freq[kMaxHalfDim];   // RoPE frequencies theta_j = base^(-2j/d), host-computed
   const int32_t *flag;      // lazy re-indexing decision (device)
   const uint16_t *sum_k, *sum_v;   // [n_layers][row_elems] staged summary rows
-  const int32_t *sum_meta;  // [n_layers][4]: insert index, stream pos, RoPE pos, evicted
+  const int32_t *sum_meta;  // [n_layers][kSumMeta]
   int32_t axes;             // 1, or 3 for M-RoPE (t, h, w)
   int32_t section[3];       // M-RoPE: frequency pairs of the t, h, w sections
   const int32_t *newc;      // M-RoPE: [n_layers][3][newc_lstride] re-indexed coordinates by output row
@@ -143,8 +146,10 @@ struct SummaryArgs {
   double *part;             // [n_layers][blocks][2 * row_elems]
   int64_t part_lstride;
   uint16_t *sum_k, *sum_v;  // [n_layers][row_elems]
-  int32_t *sum_meta;        // [n_layers][4]
+  int32_t *sum_meta;        // [n_layers][kSumMeta]
   int32_t row_elems, head_dim, n_list;
+  int32_t axes;             // 3: keys aligned to the target's (t, h, w) section by section
+  int32_t section[3];
   double inv_freq[kMaxHalfDim];   // RoPE frequencies theta_j = base^(-2j/d), host-computed
   int32_t len[kMaxLayers];      // by entry: candidates T
   int32_t budget[kMaxLayers];   // by entry: kept M
@@ -177,6 +182,7 @@ struct RankArgs {
   const LayerTable *tab;
   const int32_t *kept;
   int64_t kept_lstride;
+  const int32_t *sum_meta;  // summary rows (has_sum): insert index and (t, h, w)
   int32_t *newc;
   int64_t newc_lstride;
   const int32_t *flag;      // lazy decision (device)
@@ -187,6 +193,7 @@ struct RankArgs {
   int8_t layer_id[kMaxLayers];
   int8_t cur[kMaxLayers];
   int8_t mode[kMaxLayers];
+  int8_t has_sum[kMaxLayers];
 };
 
 // Append copy: new K/V rows and positions into rows [T0, T0 + C) of the

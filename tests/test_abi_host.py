@@ -237,7 +237,6 @@ def _sec(a, b, c):
 @pytest.mark.parametrize("over,code", [
     ({"rope_axes": 2}, H.EINVAL),
     ({"rope_axes": -1}, H.EINVAL),
-    ({"rope_axes": 3, "summary_mode": 1}, H.ENOTSUP),
     ({"rope_axes": 3, "mrope_section": _sec(8, 8, 8)}, H.EINVAL),      # sums to 24, not d/2 = 32
     ({"rope_axes": 3, "mrope_section": _sec(-1, 17, 16)}, H.EINVAL),
     ({"rope_axes": 3, "n_q_heads": 16, "n_kv_heads": 16, "head_dim": 128}, H.ENOTSUP),

@@ -360,9 +360,10 @@ def _grid(n, H, W, offset, t_step):
     return np.stack([offset + f * t_step, offset + r // W, offset + r % W], 1).astype(np.int64)
 
 
-def _mrope_case(shape, mode, section_gpu, section_oracle, t_step=2, frames=5):
+def _mrope_case(shape, mode, section_gpu, section_oracle, t_step=2, frames=5, summary=False):
     """`frames` cached frames of 14 x 14 tokens (text prefix 3) + 1 new frame;
-    the last layer keeps everything and is re-indexed in place."""
+    the last layer keeps everything and is re-indexed in place; with
+    summary, the evicting deep layer folds its evicted tokens into one."""
     Hq, Hkv, d = shape
     classes = [S, M, D, D]
     T0, C = frames * 196, 196
@@ -375,20 +376,23 @@ def _mrope_case(shape, mode, section_gpu, section_oracle, t_step=2, frames=5):
         c["thw"] = g[:T0].T.copy()
     # the largest coordinate retained anywhere is h = w = 3 + 13 = 16 (with
     # t step 2, t reaches 13)
-    limit = {"eager": 0, "lazy_fires": 18, "lazy_waits": 19}[mode]
-    ext = he.ExtConfig(reindex_mode=he.REINDEX_EAGER if mode == "eager" else he.REINDEX_LAZY,
-                       rope_offset=5, rope_limit=limit, rope_headroom=2, rope_axes=3,
-                       mrope_section=section_oracle)
+    limit = {"eager": 0, "lazy_fires": 18, "lazy_waits": 19, "none": 0}[mode]
+    rmode = {"eager": he.REINDEX_EAGER, "none": he.REINDEX_NONE}.get(mode, he.REINDEX_LAZY)
+    ext = he.ExtConfig(summary=summary, reindex_mode=rmode, rope_offset=5, rope_limit=limit,
+                       rope_headroom=2, rope_axes=3, mrope_section=section_oracle)
     say(f"mrope {shape} {mode} section {section_gpu} t step {t_step}")
     ext_caches = [he.ExtLayerCache(f64(c["k"]), f64(c["v"]), c["pos"].astype(np.int64),
                                    g[:T0, 0].copy(), g[:T0].copy()) for c in caches]
     ext_chunks = [dict(ch, rope_thw=g[T0:].T.copy()) for ch in _ext_chunks(chunks)]
     ref = he.stream_step_ext(ext_caches, ext_chunks, orc.OracleConfig(budgets=list(wl.budgets),
                                                                       classes=classes), ext)
-    assert ref["reindexed"] == (mode != "lazy_waits")
+    assert ref["reindexed"] == (mode not in ("lazy_waits", "none"))
+    if summary:
+        assert ref["summaries"][2] is not None
     kv = streaming.make_cache(wl, device="cuda", caches=caches, debug=True, layer_class=classes,
-                              reindex_mode=ext.reindex_mode, rope_offset=5, rope_limit=limit,
-                              rope_headroom=2, rope_axes=3, mrope_section=section_gpu)
+                              summary_mode=int(summary), reindex_mode=ext.reindex_mode, rope_offset=5,
+                              rope_limit=limit, rope_headroom=2, rope_axes=3,
+                              mrope_section=section_gpu)
     t = streaming.chunk_tensors(_stack(chunks), "cuda")
     thw = torch.from_numpy(np.ascontiguousarray(g[T0:].T, dtype=np.int32)).cuda()
     kv.append(t["q"], t["k"], t["v"], t["pos"], rope_thw=thw)
@@ -416,6 +420,19 @@ def test_mrope_reindex_default_section(shape):
     must be the oracle's default (16/24/24 at d = 128, 8/12/12 at d = 64);
     the benchmark's 3D re-indexing leg runs with it."""
     _mrope_case(shape, "eager", (0, 0, 0), ())
+
+
+@pytest.mark.parametrize("shape", [(14, 2, 64), (28, 4, 128), (32, 8, 128)])
+@pytest.mark.parametrize("mode", ["none", "eager", "lazy_fires"])
+def test_mrope_summary_tokens(shape, mode):
+    """Summary tokens with 3D coordinates (appendix summary algorithm with the
+    3D re-indexing's sectioned RotaryDelta): the evicting deep layer's
+    evicted keys are turned to the newest evicted token's (t, h, w) and
+    averaged; the summary row (K, V, stream position and coordinates) and,
+    with re-indexing, the ranks that now include it, against the oracle."""
+    d = shape[2]
+    section = (8, 12, 12) if d == 64 else (16, 24, 24)
+    _mrope_case(shape, mode, section, section, summary=True)
 
 
 @pytest.mark.parametrize("t_step", [70001, 300007])

@@ -335,6 +335,45 @@ def test_mrope_reindexed_keys_equal_keys_made_at_new_coordinates():
     assert np.abs(moved - made_at(x, new)).max() < 1e-12
 
 
+def test_summary3_key_is_mean_raw_key_at_the_target_coordinates():
+    """Summary token with 3D coordinates: keys made at (t, h, w)_i (complex
+    exponentials per section, computed here) and aligned to the newest
+    evicted token's coordinates average to the key made at those coordinates
+    from the mean unrotated vector; V is the plain mean; the target is the
+    last row's coordinates."""
+    d, section = 32, (4, 6, 6)
+    axis = np.array([0] * section[0] + [1] * section[1] + [2] * section[2])
+    freq = 1.0e6 ** (-np.arange(d // 2) * 2.0 / d)
+
+    def made_at(x, p):
+        z = x[..., : d // 2] + 1j * x[..., d // 2:]
+        z = z * np.exp(1j * p[:, axis][:, None, :] * freq[None, None, :])
+        return np.concatenate([z.real, z.imag], axis=-1)
+
+    g = _grid(3, 4, 4, offset=5)
+    ev = np.sort(RNG.choice(len(g), size=13, replace=False))
+    c = g[ev]
+    x = _raw(13, 2, d)
+    v = _raw(13, 2, d)
+    ks, vs, tgt = he.summary_token3(made_at(x, c), v, c, section)
+    assert np.array_equal(tgt, c[-1])
+    assert np.abs(ks - made_at(x.mean(axis=0)[None], c[-1:])[0]).max() < 1e-12
+    assert np.abs(vs - v.mean(axis=0)).max() < 1e-15
+
+
+def test_summary3_with_one_section_is_the_1d_summary_on_t():
+    """All frequency pairs in the t section: the 3D summary is the 1D summary
+    over the t coordinates (h and w play no part)."""
+    k, v = _raw(9, 2, 16), _raw(9, 2, 16)
+    t = np.sort(RNG.choice(3000, 9, replace=False))
+    c = np.stack([t, RNG.integers(0, 50, 9), RNG.integers(0, 50, 9)], 1)
+    ks3, vs3, tgt = he.summary_token3(k, v, c, (8, 0, 0))
+    ks1, vs1, t1 = he.summary_token(k, v, t)
+    assert tgt[0] == t1 and np.array_equal(ks3, ks1) and np.array_equal(vs3, vs1)
+    ks_one, vs_one, tgt_one = he.summary_token3(k[:1], v[:1], c[:1], (4, 2, 2))
+    assert np.array_equal(ks_one, k[0]) and np.array_equal(vs_one, v[0]) and np.array_equal(tgt_one, c[0])
+
+
 def _tiny_mrope(L=3, frames0=4, frames=1, H=3, W=4, Hq=4, Hkv=2, d=16, budgets=(30, 30, 30), seed=5):
     rng = np.random.default_rng(seed)
     r = lambda *s: he.round_to_bf16(rng.standard_normal(s) * 0.5)
@@ -369,3 +408,28 @@ def test_ext_step_mrope_eager_and_lazy():
     assert not no["reindexed"] and yes["reindexed"]
     for l in range(3):
         assert np.array_equal(yes["caches"][l].k, res["caches"][l].k)
+
+
+def test_ext_step_mrope_with_summary_tokens():
+    """3D coordinates with summary tokens: every evicting deep layer holds
+    budget + 1 rows, the summary at the sorted place of the newest evicted
+    token with that token's stream position and (t, h, w); eager re-indexing
+    then ranks the summary's coordinates with the kept rows'."""
+    caches, chunks, cfg, g = _tiny_mrope(budgets=(30, 30, 30))
+    ext = he.ExtConfig(summary=True, rope_axes=3)
+    res = he.stream_step_ext(caches, chunks, cfg, ext)
+    cat = res["appended"][2]
+    summ = res["summaries"][2]
+    assert summ is not None and res["summaries"][0] is None and res["summaries"][1] is None
+    c = res["caches"][2]
+    assert len(c.pos) == 31
+    newest = summ["source"]
+    assert newest == summ["evicted"][-1]
+    assert np.array_equal(c.rpos3[summ["index"]], cat.rpos3[newest])
+    assert c.pos[summ["index"]] == cat.pos[newest] and np.all(np.diff(c.pos) > 0)
+    assert np.array_equal(summ["target"], cat.rpos3[newest])
+    eager = he.stream_step_ext(caches, chunks, cfg, he.ExtConfig(summary=True, rope_axes=3,
+                                                                reindex_mode=he.REINDEX_EAGER,
+                                                                rope_offset=3))
+    e = eager["caches"][2]
+    assert np.array_equal(e.rpos3, he.reindex_coords3(c.rpos3, 3))
