@@ -71,50 +71,30 @@ __device__ __forceinline__ int xcd_remap(int i, int n) {
   return x < r ? x * (q + 1) + k : r * (q + 1) + (x - r) * q + k;
 }
 
-// SPLIT: one key slice per workgroup, partial state out (see AttnArgs).
-// WRITE_O: store O (chunk and query passes); without it only the row LSE is
-// written (guidance-prompt passes).
-template <int D, bool SPLIT, bool WRITE_O>
+// STREAM: balanced short passes (query, guidance prompt).  The key tiles of
+// every (entry, KV head) pair, concatenated in pair order (pair k = j Hkv +
+// kv, st_tiles[j] tiles each, entry j's pairs from tile st_off[j]), are cut
+// into st_units equal ranges; unit u is nqt workgroups with consecutive ids
+// (one per query tile, sharing the K/V tiles in their XCD's L2) over tiles
+// [u N / U, (u + 1) N / U).  The workgroup walks its range in one tile loop;
+// where the range leaves a pair it writes the pair's unnormalised partial
+// state (bf16 O, fp32 running maximum and row sum) to partial block (u + k)
+// of its query tile (distinct for every (u, k): a later unit only covers
+// later pairs) and switches to the next pair.  attn_combine merges a pair's
+// blocks.  Otherwise: one workgroup per (entry, KV head, query tile) over its
+// whole sequence, writing O (WRITE_O) and the row LSE.
+template <int D, bool STREAM, bool WRITE_O>
 __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   const int lin = xcd_remap(blockIdx.x, gridDim.x);
-  // Consecutive ids: the query tiles of one (layer, KV head[, key slice]),
-  // which stream the same K/V.
-  int j, qtile, kv, split = 0, nsp = 1;
-  if constexpr (SPLIT) {
-    // entry j owns workgroups [wg_start[j], wg_start[j+1]) (uniform search)
-    j = 0;
-    while (j + 1 < kMaxLayers && lin >= a.wg_start[j + 1]) ++j;
-    const int local = lin - a.wg_start[j];
-    nsp = a.nsp[j];
-    qtile = local % nqt;
-    split = (local / nqt) % nsp;
-    kv = local / (nqt * nsp);
-  } else {
-    qtile = lin % nqt;
-    kv = (lin / nqt) % a.Hkv;
-    j = lin / (nqt * a.Hkv);
-  }
-  const int layer = a.layer_id[j];
-  const LayerTable &lt = a.tab[layer];
-  const int cur = a.cur[j];
-  const int T0 = a.T0[j];
+  const int qtile = lin % nqt;
   const int C = a.C, Hq = a.Hq, Hkv = a.Hkv;
   const int G = Hq / Hkv;
   const int P = C * G;
-  const int T = T0 + C;
   const int p0 = qtile * BM;
   if (p0 >= P) return;
 
   const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
   const int half = lane >> 5, l32 = lane & 31;
-
-  const int slot = a.slot[j];
-  const uint16_t *q = a.q + slot * a.q_lstride;
-  const uint16_t *kn = a.kn + slot * a.kv_lstride;
-  const uint16_t *vn = a.vn + slot * a.kv_lstride;
-  uint16_t *out = a.out + slot * a.q_lstride;
-  const uint16_t *kc = lt.k[cur];
-  const uint16_t *vc = lt.v[cur];
 
   // This lane's query row (column n of the S^T tile).
   const int prow = p0 + wave * 32 + l32;
@@ -124,20 +104,74 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   // barrier, but issues no MFMAs.
   const bool wave_rows = __builtin_amdgcn_readfirstlane(p0 + wave * 32 < P ? 1 : 0) != 0;
   const int r = row_ok ? prow / G : 0;
-  const int h = kv * G + (row_ok ? prow - r * G : 0);
-  const int vis = row_ok ? T0 + r : -1;     // last candidate this row sees
-  const int vis_min = T0 + p0 / G;          // every row of the block sees keys <= vis_min
-
-  bf16x8 qf[D / 16];
-#pragma unroll
-  for (int kk = 0; kk < D / 16; ++kk) {
-    qf[kk] = row_ok ? *reinterpret_cast<const bf16x8 *>(q + ((int64_t)r * Hq + h) * D + 16 * kk + 8 * half)
-                    : bf16x8{};
-  }
-
+  const int g = row_ok ? prow - r * G : 0;
   const int pmax = min(p0 + BM, P) - 1;
-  const int nkeys = T0 + pmax / G + 1;
-  const int ntiles = (nkeys + BN - 1) / BN;
+
+  // Pair state: entry j, KV head kv, its cache and new rows.
+  int j = 0, kv = 0, T0 = 0, T = 0, vis = -1, vis_min = 0, ntiles = 0, n_pure = 0, first = 0;
+  const uint16_t *q = nullptr, *kn = nullptr, *vn = nullptr, *kc = nullptr, *vc = nullptr;
+  const int64_t row_stride = (int64_t)Hkv * D;
+  constexpr int CH = D / 8;                 // 16-byte chunks per key row and head
+  constexpr int NLD = BN * CH / AT;         // chunks per thread per tensor
+  uint32_t cofs[NLD];
+  bf16x8 qf[D / 16];
+  // STREAM: this unit's tile range over the concatenated pairs
+  int x_lo = 0, x_hi = 0, u = 0;
+  if constexpr (STREAM) {
+    u = lin / nqt;
+    x_lo = (int)((int64_t)u * a.st_total / a.st_units);
+    x_hi = (int)((int64_t)(u + 1) * a.st_total / a.st_units);
+    if (x_lo >= x_hi) return;
+  }
+  auto enter = [&](int jj, int kvv) {
+    j = jj;
+    kv = kvv;
+    const LayerTable &lt = a.tab[a.layer_id[j]];
+    const int cur = a.cur[j];
+    T0 = a.T0[j];
+    T = T0 + C;
+    vis = row_ok ? T0 + r : -1;             // last candidate this row sees
+    vis_min = T0 + p0 / G;                  // every row of the block sees keys <= vis_min
+    const int nkeys = T0 + pmax / G + 1;
+    ntiles = (nkeys + BN - 1) / BN;
+    // tiles [0, n_pure) lie wholly in the cache and below every row's causal
+    // limit: they load with plain pointer strides and need no mask
+    n_pure = min(ntiles, T0 / BN);
+    const int slot = a.slot[j];
+    q = a.q + slot * a.q_lstride;
+    kn = a.kn + slot * a.kv_lstride;
+    vn = a.vn + slot * a.kv_lstride;
+    kc = lt.k[cur];
+    vc = lt.v[cur];
+    const int h = kv * G + g;
+#pragma unroll
+    for (int kk = 0; kk < D / 16; ++kk) {
+      qf[kk] = row_ok ? *reinterpret_cast<const bf16x8 *>(q + ((int64_t)r * Hq + h) * D + 16 * kk + 8 * half)
+                      : bf16x8{};
+    }
+    // byte offset of this thread's chunk u inside a key tile of the cache; a
+    // pure tile's loads are then a uniform base plus this 32-bit offset
+#pragma unroll
+    for (int uu = 0; uu < NLD; ++uu) {
+      const int e = tid + uu * AT;
+      cofs[uu] = (uint32_t)(((e / CH) * row_stride + kv * D + (e % CH) * 8) * sizeof(uint16_t));
+    }
+  };
+  // the pair holding concatenated tile x (STREAM), its first tile in `first`
+  auto locate = [&](int x, int &jj, int &kvv, int &f) {
+    int e = 0;
+    while (e + 1 < a.st_entries && x >= a.st_off[e + 1]) ++e;
+    jj = e;
+    kvv = (x - a.st_off[e]) / a.st_tiles[e];
+    f = a.st_off[e] + kvv * a.st_tiles[e];
+  };
+  if constexpr (STREAM) {
+    int jj, kvv;
+    locate(x_lo, jj, kvv, first);
+    enter(jj, kvv);
+  } else {
+    enter(lin / (nqt * Hkv), (lin / nqt) % Hkv);
+  }
 
   // Double-buffered K and V tiles, both row-major [key][d]; V is read
   // transposed by ds_read_b64_tr_b16.  Row pads keep the K reads (16 B per
@@ -145,54 +179,42 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   // over the LDS banks.
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN][D + KPAD];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN][D + VPAD];
-
-  constexpr int CH = D / 8;                 // 16-byte chunks per key row and head
-  constexpr int NLD = BN * CH / AT;         // chunks per thread per tensor
-  const int64_t row_stride = (int64_t)Hkv * D;
   uint4 kreg[NLD], vreg[NLD];
-  // Tiles [0, n_pure) lie wholly in the cache and below every row's causal
-  // limit: they load with plain pointer strides and need no mask.
-  const int n_pure = min(ntiles, T0 / BN);
-  // byte offset of this thread's chunk u inside a key tile of the cache; a
-  // pure tile's loads are then a uniform base plus this 32-bit offset
-  uint32_t cofs[NLD];
-#pragma unroll
-  for (int u = 0; u < NLD; ++u) {
-    const int e = tid + u * AT;
-    cofs[u] = (uint32_t)(((e / CH) * row_stride + kv * D + (e % CH) * 8) * sizeof(uint16_t));
-  }
   auto load_pure = [&](int k0) {
     const char *kb = reinterpret_cast<const char *>(kc + (int64_t)k0 * row_stride);
     const char *vb = reinterpret_cast<const char *>(vc + (int64_t)k0 * row_stride);
 #pragma unroll
-    for (int u = 0; u < NLD; ++u) {
-      kreg[u] = gload16(reinterpret_cast<const uint16_t *>(kb + cofs[u]));
-      vreg[u] = gload16(reinterpret_cast<const uint16_t *>(vb + cofs[u]));
+    for (int uu = 0; uu < NLD; ++uu) {
+      kreg[uu] = gload16(reinterpret_cast<const uint16_t *>(kb + cofs[uu]));
+      vreg[uu] = gload16(reinterpret_cast<const uint16_t *>(vb + cofs[uu]));
     }
   };
-  auto load_any = [&](int k0) {
+  // a tile of any pair (its cache, new rows, lengths and KV head given)
+  auto load_from = [&](int k0, const uint16_t *kcx, const uint16_t *vcx, const uint16_t *knx,
+                       const uint16_t *vnx, int T0x, int Tx, int kvx) {
 #pragma unroll
-    for (int u = 0; u < NLD; ++u) {
-      const int e = tid + u * AT;
+    for (int uu = 0; uu < NLD; ++uu) {
+      const int e = tid + uu * AT;
       const int kr = e / CH, ch = e % CH;
       const int i = k0 + kr;
       uint4 k4 = {0u, 0u, 0u, 0u}, v4 = {0u, 0u, 0u, 0u};
-      if (i < T) {
-        const int64_t off = (i < T0 ? (int64_t)i : (int64_t)(i - T0)) * row_stride + kv * D + ch * 8;
-        k4 = gload16((i < T0 ? kc : kn) + off);
-        v4 = gload16((i < T0 ? vc : vn) + off);
+      if (i < Tx) {
+        const int64_t off = (i < T0x ? (int64_t)i : (int64_t)(i - T0x)) * row_stride + kvx * D + ch * 8;
+        k4 = gload16((i < T0x ? kcx : knx) + off);
+        v4 = gload16((i < T0x ? vcx : vnx) + off);
       }
-      kreg[u] = k4;
-      vreg[u] = v4;
+      kreg[uu] = k4;
+      vreg[uu] = v4;
     }
   };
+  auto load_any = [&](int k0) { load_from(k0, kc, vc, kn, vn, T0, T, kv); };
   auto store_tile = [&](int b) {
 #pragma unroll
-    for (int u = 0; u < NLD; ++u) {
-      const int e = tid + u * AT;
+    for (int uu = 0; uu < NLD; ++uu) {
+      const int e = tid + uu * AT;
       const int kr = e / CH, ch = e % CH;
-      *reinterpret_cast<uint4 *>(&Ks[b][kr][ch * 8]) = kreg[u];
-      *reinterpret_cast<uint4 *>(&Vs[b][kr][ch * 8]) = vreg[u];
+      *reinterpret_cast<uint4 *>(&Ks[b][kr][ch * 8]) = kreg[uu];
+      *reinterpret_cast<uint4 *>(&Vs[b][kr][ch * 8]) = vreg[uu];
     }
   };
 
@@ -207,8 +229,12 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   const int tr_row = 4 * (g16 >> 1) + (s16 >> 2);
   const int tr_col = 16 * (g16 & 1) + 4 * (s16 & 3);
 
-  auto compute = [&](int t, auto masked) {
-    const int b = t & 1;
+  // key tile t (keys from k0 = t * BN) of the current pair, in LDS buffer b.
+  // `masked` is a std::integral_constant in the plain kernel's loops (the
+  // mask code folds away per call site) and a uniform bool in stream mode,
+  // whose single instance of this body fits the register budget (two
+  // instances in one loop spill).
+  auto compute = [&](int b, int t, auto masked) {
     const int k0 = t * BN;
     // S^T = K Q^T for two 32-key sub-tiles: lane = query row, register = key.
     f32x16 s[2];
@@ -233,7 +259,7 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
     }
 #pragma unroll
     for (int i = 0; i < kAheadK; ++i) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-    if constexpr (decltype(masked)::value) {
+    if (masked) {
 #pragma unroll
       for (int sub = 0; sub < 2; ++sub) {
 #pragma unroll
@@ -310,67 +336,13 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
 
   using NoMask = std::integral_constant<bool, false>;
   using Mask = std::integral_constant<bool, true>;
-  // Steady state: the tile and the next one are pure (no branch in the
-  // body); the last pure tile joins the general loop, where it is unmasked.
-  if constexpr (!SPLIT) {
-    if (n_pure > 0) load_pure(0); else load_any(0);
-    int t = 0;
-    for (; t + 1 < n_pure; ++t) {
-      store_tile(t & 1);
-      __syncthreads();
-      load_pure((t + 1) * BN);
-      if (wave_rows) compute(t, NoMask{});
-    }
-    for (; t < ntiles; ++t) {
-      store_tile(t & 1);
-      __syncthreads();
-      if (t + 1 < ntiles) load_any((t + 1) * BN);
-      if (!wave_rows) {
-      } else if ((t + 1) * BN - 1 > vis_min) {
-        compute(t, Mask{});
-      } else {
-        compute(t, NoMask{});
-      }
-    }
-  } else {
-    // this workgroup's slice [t_begin, t_end) of the key tiles
-    const int tps = (ntiles + nsp - 1) / nsp;
-    const int t_begin = min(ntiles, split * tps);
-    const int t_end = min(ntiles, t_begin + tps);
-    const int p_end = min(n_pure, t_end);
-    int t = t_begin;
-    if (t < t_end) {
-      if (t < p_end) load_pure(t * BN); else load_any(t * BN);
-    }
-    for (; t + 1 < p_end; ++t) {
-      store_tile(t & 1);
-      __syncthreads();
-      load_pure((t + 1) * BN);
-      if (wave_rows) compute(t, NoMask{});
-    }
-    for (; t < t_end; ++t) {
-      store_tile(t & 1);
-      __syncthreads();
-      if (t + 1 < t_end) load_any((t + 1) * BN);
-      if (!wave_rows) {
-      } else if ((t + 1) * BN - 1 > vis_min) {
-        compute(t, Mask{});
-      } else {
-        compute(t, NoMask{});
-      }
-    }
-  }
-
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if constexpr (SPLIT) {
-    // unnormalised partial state of this key slice
+  // unnormalised partial state of the current pair into partial block blk:
+  // bf16 O (half the bytes the combine reads back), fp32 running maximum and
+  // row sum (they fix the LSE)
+  auto flush = [&](int64_t blk) {
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
     if (row_ok) {
-      // partial block of (entry j, KV head kv, slice split): entry j's blocks
-      // start after the Hkv * nsp blocks of every earlier entry
-      const int64_t blk = a.wg_start[j] / nqt + (int64_t)kv * nsp + split;
       const int64_t row = blk * a.part_rows + prow;
-      // bf16 halves the state the combine reads back; the maximum and the
-      // row sum, which fix the LSE, stay fp32
       uint16_t *op = a.opart + row * D;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db)
@@ -383,45 +355,112 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
         }
       if (half == 0) *reinterpret_cast<float2 *>(a.mlpart + 2 * row) = float2{m_run, l_tot};
     }
+  };
+  if constexpr (STREAM) {
+    // One tile loop over the range; leaving a pair (rare) flushes it, moves
+    // to the next pair and loads that pair's first tile without prefetch.
+    int t = x_lo - first;
+    int pair_n = a.st_tiles[j];
+    int k = j * Hkv + kv;
+    if (t < n_pure) load_pure(t * BN); else load_any(t * BN);
+    int b = 0;
+    for (int x = x_lo; x < x_hi; ++x) {
+      store_tile(b);
+      __syncthreads();
+      const bool pair_end = t + 1 == pair_n;
+      if (!pair_end && x + 1 < x_hi) {
+        if (t + 1 < n_pure) load_pure((t + 1) * BN); else load_any((t + 1) * BN);
+      }
+      // tiles past this query tile's own causal limit hold no visible key
+      if (wave_rows && t < ntiles) compute(b, t, (t + 1) * BN - 1 > vis_min);
+      if (pair_end && x + 1 < x_hi) {
+        flush(u + k);
+        if (kv + 1 < Hkv) enter(j, kv + 1); else enter(j + 1, 0);
+        pair_n = a.st_tiles[j];
+        ++k;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
+        m_run = -1e30f;
+        l_run = 0.f;
+        t = 0;
+        if (n_pure > 0) load_pure(0); else load_any(0);
+      } else {
+        ++t;
+      }
+      b ^= 1;
+    }
+    flush(u + k);
     return;
-  }
-  const float inv = 1.f / l_tot;
-  if (row_ok) {
-    if constexpr (WRITE_O) {
-      uint16_t *orow = out + ((int64_t)r * Hq + h) * D;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-#pragma unroll
-        for (int grp = 0; grp < 4; ++grp) {
-          const int d0 = 32 * db + 8 * grp + 4 * half;
-          const uint32_t w0 = (uint32_t)f2bf(o[db][4 * grp + 0] * inv) |
-                              ((uint32_t)f2bf(o[db][4 * grp + 1] * inv) << 16);
-          const uint32_t w1 = (uint32_t)f2bf(o[db][4 * grp + 2] * inv) |
-                              ((uint32_t)f2bf(o[db][4 * grp + 3] * inv) << 16);
-          *reinterpret_cast<uint2 *>(orow + d0) = uint2{w0, w1};
-        }
+  } else {
+    // Steady state: the tile and the next one are pure (no branch in the
+    // body); the last pure tile joins the general loop, where it is unmasked.
+    if (n_pure > 0) load_pure(0); else load_any(0);
+    int t = 0;
+    for (; t + 1 < n_pure; ++t) {
+      store_tile(t & 1);
+      __syncthreads();
+      load_pure((t + 1) * BN);
+      if (wave_rows) compute(t & 1, t, NoMask{});
+    }
+    for (; t < ntiles; ++t) {
+      store_tile(t & 1);
+      __syncthreads();
+      if (t + 1 < ntiles) load_any((t + 1) * BN);
+      if (!wave_rows) {
+      } else if ((t + 1) * BN - 1 > vis_min) {
+        compute(t & 1, t, Mask{});
+      } else {
+        compute(t & 1, t, NoMask{});
       }
     }
-    if (a.lse != nullptr && half == 0) {
-      a.lse[layer * a.lse_lstride + (int64_t)kv * P + prow] = m_run + log2f(l_tot);
+
+    const float l_tot = l_run + __shfl_xor(l_run, 32);
+    const float inv = 1.f / l_tot;
+    if (row_ok) {
+      if constexpr (WRITE_O) {
+        uint16_t *orow = a.out + a.slot[j] * a.q_lstride + ((int64_t)r * Hq + kv * G + g) * D;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+          for (int grp = 0; grp < 4; ++grp) {
+            const int d0 = 32 * db + 8 * grp + 4 * half;
+            const uint32_t w0 = (uint32_t)f2bf(o[db][4 * grp + 0] * inv) |
+                                ((uint32_t)f2bf(o[db][4 * grp + 1] * inv) << 16);
+            const uint32_t w1 = (uint32_t)f2bf(o[db][4 * grp + 2] * inv) |
+                                ((uint32_t)f2bf(o[db][4 * grp + 3] * inv) << 16);
+            *reinterpret_cast<uint2 *>(orow + d0) = uint2{w0, w1};
+          }
+        }
+      }
+      if (a.lse != nullptr && half == 0) {
+        a.lse[a.layer_id[j] * a.lse_lstride + (int64_t)kv * P + prow] = m_run + log2f(l_tot);
+      }
     }
   }
 }
 
 
-// Merge of the key slices: m = max_s m_s, w_s = 2^(m_s - m),
-// O = sum_s w_s O_s / sum_s w_s l_s, LSE = m + log2(sum_s w_s l_s).
-// One thread per (packed row, 8 channels), slices summed in order.
+// Merge of a pair's partial blocks: m = max_s m_s, w_s = 2^(m_s - m),
+// O = sum_s w_s O_s / sum_s w_s l_s, LSE = m + log2(sum_s w_s l_s).  Pair
+// k = j Hkv + kv covers concatenated tiles [f, f + n); units u0 (holding
+// tile f) to u1 (holding tile f + n - 1) wrote its blocks u0 + k .. u1 + k.
+// One thread per (packed row, 8 channels), blocks summed in order.
 template <int D>
 __global__ __launch_bounds__(256) void attn_combine(AttnArgs a) {
   const int j = blockIdx.z, kv = blockIdx.y;
   const int layer = a.layer_id[j];
-  const int G = a.Hq / a.Hkv, P = a.C * G, nsp = a.nsp[j];
+  const int G = a.Hq / a.Hkv, P = a.C * G;
   const int e = blockIdx.x * 256 + threadIdx.x;
   if (e >= P * (D / 8)) return;
   const int p = e / (D / 8), c8 = e % (D / 8);
-  const int nqt = (P + BM - 1) / BM;
-  const int64_t row0 = (a.wg_start[j] / nqt + (int64_t)kv * nsp) * a.part_rows + p;
+  // the unit whose range [u N / U, (u + 1) N / U) holds tile x
+  auto unit_of = [&](int64_t x) {
+    return (int)(((x + 1) * a.st_units + a.st_total - 1) / a.st_total - 1);
+  };
+  const int64_t f = a.st_off[j] + (int64_t)kv * a.st_tiles[j];
+  const int u0 = unit_of(f);
+  const int nsp = unit_of(f + a.st_tiles[j] - 1) - u0 + 1;
+  const int64_t row0 = ((int64_t)u0 + j * a.Hkv + kv) * a.part_rows + p;
   float m = -INFINITY;
   for (int s = 0; s < nsp; ++s) m = fmaxf(m, a.mlpart[2 * (row0 + (int64_t)s * a.part_rows)]);
   float lsum = 0.f, acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
@@ -702,10 +741,10 @@ hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStre
   return hipGetLastError();
 }
 
-hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, hipStream_t s) {
+hipError_t launch_attention_stream(const AttnArgs &a, int n_list, int head_dim, hipStream_t s) {
   const int P = a.C * (a.Hq / a.Hkv);
   const int nqt = (P + BM - 1) / BM;
-  dim3 grid(a.wg_start[n_list]);
+  dim3 grid(a.st_units * nqt);
   dim3 cgrid((P * (head_dim / 8) + 255) / 256, a.Hkv, n_list);
   if (head_dim == 64) {
     hipLaunchKernelGGL((attn_fwd<64, true, true>), grid, dim3(AT), 0, s, a, nqt);

@@ -81,9 +81,9 @@ int check_config(const hermes_config *c) {
   return HERMES_OK;
 }
 
-// Workspace layout of `c`; part_blocks < 0 sizes the key-slice partial state
-// for the most slices any query can take (every layer and KV head cut into
-// kMaxSplits slices), else for that many partial blocks.
+// Workspace layout of `c`; part_blocks < 0 sizes the stream-mode partial
+// state for the most blocks any short pass can write (one per unit plus one
+// per (layer, KV head) pair), else for that many partial blocks.
 Layout layout_of(const hermes_config *c, int64_t part_blocks = -1) {
   Layout s;
   s.lse_lstride = (int64_t)c->n_q_heads * c->max_chunk;
@@ -123,9 +123,9 @@ Layout layout_of(const hermes_config *c, int64_t part_blocks = -1) {
   off = round_up(off + sizeof(int32_t) * kSumMeta * (size_t)c->n_layers);
   s.flag = off;
   off = round_up(off + sizeof(int32_t) * 4);
-  // split-key partial state of short passes (query, guidance prompt)
+  // stream-mode partial state of short passes (query, guidance prompt)
   s.part_rows = kSplitMaxTokens * (c->n_q_heads / c->n_kv_heads);
-  s.part_blocks = part_blocks >= 0 ? part_blocks : (int64_t)c->n_layers * c->n_kv_heads * kMaxSplits;
+  s.part_blocks = part_blocks >= 0 ? part_blocks : (int64_t)c->n_layers * c->n_kv_heads + kStreamSlots;
   const size_t prow = (size_t)s.part_blocks * s.part_rows;
   s.opart = off;
   off = round_up(off + sizeof(uint16_t) * prow * c->head_dim);
@@ -155,68 +155,45 @@ bool layout_within(const hermes_config *c, size_t limit, Layout *out) {
   return true;
 }
 
-// Key slices of a short pass (n_rows <= kSplitMaxTokens rows per entry over
-// caches of at.T0[j] tokens): entry j's key tiles are cut into nsp[j] slices
-// of at most m tiles (at least 8 tiles, at most kMaxSplits slices), with the
-// m that minimises rounds(m) * (longest slice + fixed work) + the combine's
-// cost, where rounds(m) is the number of 256-workgroup rounds (one attention
-// workgroup per CU) the slices take; slicing is used only when it promises at
-// least 10% over the plain kernel.  Without slicing, one workgroup per
-// (entry, KV head, query tile) runs over its whole cache, so the entry with
-// the longest cache sets the time while the others' CUs idle.  Fills nsp,
-// wg_start and nsplit (the largest nsp; 1 means the plain kernel).
-void split_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D, int64_t max_blocks) {
+// Stream plan of a short pass (n_rows <= kSplitMaxTokens rows per entry over
+// caches of at.T0[j] tokens).  The plain kernel runs one workgroup per
+// (entry, KV head, query tile) over its whole cache, so the entry with the
+// longest cache sets the time while the other CUs idle.  Stream mode cuts
+// the concatenated key tiles of all pairs into U equal ranges, U units of
+// nqt workgroups filling one round of kStreamSlots, so every CU gets the same
+// number of tiles; it pays a partial write per (unit, pair) touched and the
+// combine launch.  Costs in key-tile times: a round also pays about two
+// tiles of fixed work (query load, epilogue), the combine about two, and the
+// partial writes about one tile per 64 * 128 / D workgroup blocks.  Stream
+// mode is used when it promises at least 10% over the plain kernel and the
+// workspace holds its U + pairs - 1 partial blocks.  Fills the st_* fields
+// (st_units = 0 for the plain kernel).
+void stream_plan(AttnArgs &at, int n_rows, int G, int Hkv, int n_list, int D, int64_t max_blocks) {
   const int nqt = (n_rows * G + kAttnRowsPerBlock - 1) / kAttnRowsPerBlock;
-  std::vector<int> tiles(n_list);
+  at.st_units = 0;
+  at.st_entries = n_list;
+  int64_t total = 0;
   int max_tiles = 1;
   for (int j = 0; j < n_list; ++j) {
-    tiles[j] = (at.T0[j] + n_rows + 63) / 64;
-    max_tiles = tiles[j] > max_tiles ? tiles[j] : max_tiles;
+    const int tiles = (at.T0[j] + n_rows + 63) / 64;
+    at.st_tiles[j] = tiles;
+    at.st_off[j] = (int32_t)total;
+    total += (int64_t)Hkv * tiles;
+    max_tiles = tiles > max_tiles ? tiles : max_tiles;
   }
-  // Costs in key-tile times: a round of workgroups also pays about two tiles
-  // of fixed work (query load, epilogue); slices add the combine launch and
-  // the write and read of each workgroup's bf16 partial O (about one tile per
-  // 64 * 128 / D workgroups).
-  auto rounds = [](int64_t w) { return (double)((w + 255) / 256); };
-  double best = 0.9 * rounds((int64_t)nqt * Hkv * n_list) * (max_tiles + 2.0);
-  int best_m = 0;
-  if (n_rows <= kSplitMaxTokens) {
-    // every slice length up to 64 tiles, then steps of m / 16 (a few hundred
-    // candidates even for million-token caches)
-    for (int m = 8; m < max_tiles; m += m < 64 ? 1 : m / 16) {
-      int64_t w = 0;
-      int longest = 0, most = 1;
-      for (int j = 0; j < n_list; ++j) {
-        int ns = (tiles[j] + m - 1) / m;
-        ns = ns < kMaxSplits ? ns : kMaxSplits;
-        most = ns > most ? ns : most;
-        w += (int64_t)nqt * Hkv * ns;
-        const int len = (tiles[j] + ns - 1) / ns;
-        longest = len > longest ? len : longest;
-      }
-      if (most == 1) continue;
-      int64_t blocks = 0;   // partial blocks: one per (entry, KV head, slice)
-      for (int j = 0; j < n_list; ++j) {
-        const int ns = (tiles[j] + m - 1) / m;
-        blocks += (int64_t)Hkv * (ns < kMaxSplits ? ns : kMaxSplits);
-      }
-      if (blocks > max_blocks) continue;
-      const double cost = rounds(w) * (longest + 2.0) + 2.0 + (double)w * D / (64.0 * 128.0);
-      if (cost < best) {
-        best = cost;
-        best_m = m;
-      }
-    }
-  }
-  at.nsplit = 1;
-  at.wg_start[0] = 0;
-  for (int j = 0; j < n_list; ++j) {
-    int ns = best_m > 0 ? (tiles[j] + best_m - 1) / best_m : 1;
-    ns = ns < kMaxSplits ? ns : kMaxSplits;
-    at.nsp[j] = (int8_t)ns;
-    at.nsplit = ns > at.nsplit ? ns : at.nsplit;
-    at.wg_start[j + 1] = at.wg_start[j] + nqt * Hkv * ns;
-  }
+  at.st_off[n_list] = (int32_t)total;
+  at.st_total = (int32_t)total;
+  if (n_rows > kSplitMaxTokens || total > INT32_MAX / 2) return;
+  const int64_t pairs = (int64_t)n_list * Hkv;
+  int64_t units = kStreamSlots / nqt;
+  units = units < total ? units : total;
+  units = units < max_blocks - pairs + 1 ? units : max_blocks - pairs + 1;
+  if (units < 2) return;
+  auto rounds = [](int64_t w) { return (double)((w + kStreamSlots - 1) / kStreamSlots); };
+  const double plain = rounds((int64_t)nqt * pairs) * (max_tiles + 2.0);
+  const double per_unit = (double)((total + units - 1) / units);
+  const double stream = per_unit + 2.0 + 2.0 + (double)(units + pairs) * nqt * D / (64.0 * 128.0);
+  if (stream < 0.9 * plain) at.st_units = (int32_t)units;
 }
 
 // RoPE frequencies theta_j = base^(-2j/d), j < d/2 (rotate-half pairs), in
@@ -857,13 +834,13 @@ int hermes_guidance_score(hermes_ctx *ctx, int32_t layer, const void *q, const v
     max_T = ctx->len[l] > max_T ? ctx->len[l] : max_T;
   }
   const int n = (int)list.size();
-  split_plan(at, n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D, ctx->lay.part_blocks);
+  stream_plan(at, n_rows, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D, ctx->lay.part_blocks);
   at.part_rows = ctx->lay.part_rows;
   at.opart = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
   const int rc = ctx->run(HERMES_K_GUIDE, s, [&] {
-    hipError_t e = at.nsplit > 1 ? launch_attention_split(at, n, ctx->D, s)
-                                 : launch_attention(at, n, ctx->D, s);
+    hipError_t e = at.st_units > 0 ? launch_attention_stream(at, n, ctx->D, s)
+                                   : launch_attention(at, n, ctx->D, s);
     if (e != hipSuccess) return e;
     return launch_colsum(cs, n, max_T, ctx->D, s);
   });
@@ -1104,13 +1081,13 @@ int hermes_query_attend(hermes_ctx *ctx, int32_t layer, const void *q, const voi
     at.cur[n] = ctx->cur[l];
     ++n;
   }
-  split_plan(at, n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D, ctx->lay.part_blocks);
+  stream_plan(at, n_q, ctx->Hq / ctx->Hkv, ctx->Hkv, n, ctx->D, ctx->lay.part_blocks);
   at.part_rows = ctx->lay.part_rows;
   at.opart = reinterpret_cast<uint16_t *>(ctx->ws + ctx->lay.opart);
   at.mlpart = reinterpret_cast<float *>(ctx->ws + ctx->lay.mlpart);
   return ctx->run(HERMES_K_QUERY, s, [&] {
-    return at.nsplit > 1 ? launch_attention_split(at, n, ctx->D, s)
-                         : launch_attention(at, n, ctx->D, s);
+    return at.st_units > 0 ? launch_attention_stream(at, n, ctx->D, s)
+                           : launch_attention(at, n, ctx->D, s);
   });
 }
 

@@ -53,15 +53,17 @@ struct AttnArgs {
   int8_t layer_id[kMaxLayers];
   int8_t slot[kMaxLayers];      // index of the layer's inputs in the stacked tensors
   int8_t cur[kMaxLayers];
-  // Split-key mode (short passes): entry j's key tiles are cut into nsp[j]
-  // slices (at most kMaxSplits; nsplit is the largest), workgroups
-  // [wg_start[j], wg_start[j+1]) cover entry j, and each writes unnormalised
-  // O (bf16), the running maximum and the row sum (fp32) of its slice to
-  // opart / mlpart [block][part_rows], block = (Hkv * nsp of the earlier
-  // entries) + kv * nsp[j] + slice; a combine kernel merges the slices.
-  int32_t nsplit, part_rows;
-  int8_t nsp[kMaxLayers];
-  int32_t wg_start[kMaxLayers + 1];
+  // Stream mode (short passes): the key tiles of every (entry, KV head) pair,
+  // concatenated in pair order (entry j's Hkv pairs of st_tiles[j] tiles each
+  // start at tile st_off[j]; st_total tiles in all), are cut into st_units
+  // equal ranges of nqt workgroups each.  Unit u writes the unnormalised O
+  // (bf16), running maximum and row sum (fp32) of each pair k it touches to
+  // opart / mlpart block u + k ([block][part_rows]); a combine kernel merges
+  // each pair's blocks.  st_units = 0: the plain kernel, one workgroup per
+  // (entry, KV head, query tile).
+  int32_t st_units, st_total, st_entries, part_rows;
+  int32_t st_off[kMaxLayers + 1];
+  int32_t st_tiles[kMaxLayers];
   uint16_t *opart;          // [..][part_rows][d] bf16 (unnormalised; its scale is in mlpart)
   float *mlpart;            // [..][part_rows][2] fp32 (max, sum)
 };
@@ -223,7 +225,7 @@ void static_workspace_release(int device);
 
 // Launchers (return the hipError_t of the launch).
 hipError_t launch_attention(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);
-hipError_t launch_attention_split(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);
+hipError_t launch_attention_stream(const AttnArgs &a, int n_list, int head_dim, hipStream_t s);
 hipError_t launch_colsum(const ColsumArgs &a, int n_list, int max_T, int head_dim,
                          hipStream_t s);
 hipError_t launch_select(const SelectArgs &a, hipStream_t s);
@@ -257,8 +259,8 @@ hipError_t launch_mrope_rank(const RankArgs &a, hipStream_t s);
 constexpr int kAttnRowsPerBlock = 256;   // packed (row, head) pairs per attention workgroup
 constexpr int kColsumKeysPerBlock = 256; // candidates per workgroup of the sweep
 constexpr int kSummaryRows = 128;        // candidates per workgroup of the summary sums
-constexpr int kSplitMaxTokens = 64;      // passes of at most this many rows use split keys
-constexpr int kMaxSplits = 8;
+constexpr int kSplitMaxTokens = 64;      // passes of at most this many rows use stream mode
+constexpr int kStreamSlots = 256;        // resident attention workgroups (one per CU)
 constexpr int kNormBlock = 256;         // candidates per fp64 partial of the score normaliser
 
 }  // namespace hermes
