@@ -194,9 +194,10 @@ int hermes_kv_init(const hermes_config *cfg, const hermes_layer_buffers *layers,
  * device returns HERMES_ESTATE while the first is alive, since both would
  * share (and race on) the one array; nothing in it needs to start at zero
  * (every word is written before it is read).  When the configuration's
- * workspace (hermes_workspace_bytes) exceeds the scratch, the key-slice
- * partial state of queries and guidance prompts is cut to what fits (queries
- * then take fewer or no key slices: same results up to rounding order);
+ * workspace (hermes_workspace_bytes) exceeds the scratch, the stream-mode
+ * partial state of queries and guidance prompts is cut to what fits (those
+ * passes then use fewer stream units, or one workgroup per layer, KV head and
+ * query tile: same results up to rounding order);
  * HERMES_ECAPACITY when even the rest exceeds it.  Errors otherwise as
  * hermes_kv_init (ENOTSUP also beyond 64 devices).
  */

@@ -28,7 +28,7 @@ struct Layout {
   int64_t lse_lstride, keys_lstride, kept_lstride, wpart_lstride, spart_lstride, normpart_lstride,
       newc_lstride;
   int32_t part_rows;
-  int64_t part_blocks;      // key-slice partial blocks of part_rows rows the workspace holds
+  int64_t part_blocks;      // stream-mode partial blocks of part_rows rows the workspace holds
 };
 
 int max_budget(const hermes_config *c) {
@@ -136,9 +136,9 @@ Layout layout_of(const hermes_config *c, int64_t part_blocks = -1) {
 }
 
 // The layout of `c` in at most `limit` bytes: the default one if it fits,
-// else the same with as many key-slice partial blocks as the rest leaves
-// (possibly none: queries then run unsliced).  false if even that exceeds
-// `limit`.
+// else the same with as many stream-mode partial blocks as the rest leaves
+// (possibly none: short passes then run the plain kernel).  false if even
+// that exceeds `limit`.
 bool layout_within(const hermes_config *c, size_t limit, Layout *out) {
   const Layout full = layout_of(c);
   if (full.total <= limit) {

@@ -74,7 +74,7 @@ def _init(cfg, bufs, ws=FAKE, nbytes=None):
 
 def test_static_init_rejects_workspaces_beyond_the_scratch():
     """hermes_kv_init_static refuses a configuration whose workspace, even
-    without the key-slice partial state, exceeds the library's static device
+    without the stream-mode partial state, exceeds the library's static device
     scratch; the size check runs before any device call."""
     cfg = _cfg(max_cap=1 << 22)
     need = H.lib.hermes_workspace_bytes(ctypes.byref(cfg))

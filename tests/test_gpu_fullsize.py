@@ -266,7 +266,8 @@ def test_c3_sharp_attention_step_and_query():
     compress and the 64-token query, in the benchmark's launch configuration.
     The oracle checks the chunk attention and the attention mass of a middle
     and a deep layer, and the query output of the shortest and longest
-    compacted layers (the query's key slices are merged by the combine)."""
+    compacted layers (the query runs in stream mode, its partial states merged
+    by the combine)."""
     wl = _sharp(wk.WORKLOADS["c3_7b_28layer"], 64)
     say("[c3 sharp] generating inputs")
     caches, chunks = _gen_all(wl)
@@ -302,7 +303,7 @@ def test_c3_sharp_attention_step_and_query():
 def test_c5_sharp_query_over_long_caches():
     """The long-cache workload (32768 + 3136 tokens, budgets 4096..16384) with
     planted anchors every 128th position: append + compress, then the 64-token
-    query, whose longest layers are cut into the most key slices; sampled
+    query in stream mode (its longest layers spread over the most units); sampled
     chunk rows and the query output of the shortest and longest layer against
     the oracle."""
     wl = _sharp(wk.WORKLOADS["c5_7b_long"], 128)

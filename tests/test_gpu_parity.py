@@ -155,13 +155,15 @@ def test_long_layers_past_the_lds_staging_limits():
 
 
 @pytest.mark.parametrize("anchors", [0, 61])
-def test_query_with_per_layer_key_slices(anchors):
+def test_query_stream_mode_over_unequal_caches(anchors):
     """Layers of very different cache lengths (300, 2000 and 8000 tokens): the
-    host cuts their keys into 1, 2 and 8 slices (the most it allows), whose
-    partial states the combine merges; each layer's query output against the
-    oracle's attention over that layer's cache.  With anchors every slice
-    holds tokens that dominate some rows, so a slice merged with a wrong
-    weight, or dropped, moves the output by far more than the bars."""
+    host runs the query in stream mode, the 326 key tiles of the six (layer,
+    KV head) pairs cut into 256 unit ranges, so the longest layer's keys are
+    spread over about 100 units whose partial states the combine merges; each
+    layer's query output against the oracle's attention over that layer's
+    cache.  With anchors every range holds tokens that dominate some rows, so
+    a block merged with a wrong weight, or dropped, moves the output by far
+    more than the bars."""
     from paper_2601_14724_amd import streaming
     wl = wk.custom("slices", 123, 3, 4, 2, 64, 8000, 9, (8000, 8000, 8000), query_len=9,
                    anchor_period=anchors)
@@ -180,7 +182,7 @@ def test_query_with_per_layer_key_slices(anchors):
         cache = orc.LayerCache(f64(caches[l]["k"]), f64(caches[l]["v"]),
                                caches[l]["pos"].astype(np.int64))
         want = orc.query_attention(cache, f64(qry[l]["q"]), f64(qry[l]["k"]), f64(qry[l]["v"]))
-        check_o(o[l], want, f"[slices] layer {l} ({lens[l]} cached, anchors {anchors})")
+        check_o(o[l], want, f"[stream] layer {l} ({lens[l]} cached, anchors {anchors})")
     kv.close()
 
 
