@@ -149,3 +149,46 @@ def test_precondition_checks_reject_before_any_launch(monkeypatch):
     torch.cuda.synchronize()
     assert [envkv.length(l) for l in range(3)] == [28, 28, 28]
     envkv.close()
+
+
+def test_checkpoint_resume_is_bitwise():
+    """Checkpoint / resume: after three append + compress steps the per-layer
+    state is read back through hermes_kv_view (K, V and positions of each
+    layer's current buffer, its length), copied to host memory, and a fresh
+    context is created from it (init_len = the lengths).  Three more steps on
+    the original and on the resumed context then give bit-identical outputs,
+    attention mass and compacted caches: the context holds no other state
+    that the next steps read."""
+    wl = wk.custom("resume", 131, 4, 8, 2, 64, 600, 48, (300, 400, 500, 600), n_steps=6)
+    kv = streaming.make_cache(wl, max_chunk=wl.chunk)
+    steps = [streaming.chunk_tensors(wk.stack_chunks(wl, s)) for s in range(6)]
+    for s in range(3):
+        t = steps[s]
+        kv.append(t["q"], t["k"], t["v"], t["pos"])
+        kv.compress()
+    snap = [tuple(x.cpu().clone() for x in kv.view(l)) for l in range(wl.n_layers)]
+    lens = [kv.length(l) for l in range(wl.n_layers)]
+    assert lens == [min(b, wl.init_len + 3 * wl.chunk) for b in wl.budgets]
+    init = [tuple(x.to("cuda") for x in snap[l]) for l in range(wl.n_layers)]
+    kv2 = H.HermesKV(wl.n_layers, wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.budgets,
+                     wl.chunk, cap=kv.cap, init=init)
+    assert [kv2.length(l) for l in range(wl.n_layers)] == lens
+    for s in range(3, 6):
+        t = steps[s]
+        o1 = kv.append(t["q"], t["k"], t["v"], t["pos"]).clone()
+        o2 = kv2.append(t["q"], t["k"], t["v"], t["pos"]).clone()
+        assert torch.equal(o1.view(torch.int16), o2.view(torch.int16)), f"step {s}: O differs"
+        for l in range(wl.n_layers):
+            n = kv.length(l)
+            assert torch.equal(kv.w[l][:n], kv2.w[l][:n]), f"step {s} layer {l}: W differs"
+        kv.compress()
+        kv2.compress()
+        for l in range(wl.n_layers):
+            a, b = kv.view(l), kv2.view(l)
+            assert len(a[2]) == len(b[2])
+            for x, y in zip(a, b):
+                assert torch.equal(x.view(torch.int16) if x.dtype == torch.bfloat16 else x,
+                                   y.view(torch.int16) if y.dtype == torch.bfloat16 else y), \
+                    f"step {s} layer {l}: compacted state differs"
+    kv.close()
+    kv2.close()
