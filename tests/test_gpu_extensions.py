@@ -251,9 +251,10 @@ def test_guidance_prompt_scoring():
 
 def test_guidance_prompt_all_layers_one_pass():
     """A 64-row prompt for all 28 layers of the 7B head shape in one call:
-    the row pass fills one round of workgroups, so it runs unsliced (the
-    row-LSE-only attention kernel); W, smoothed keys and kept sets against
-    the oracle."""
+    the caches are equal in length and the row pass fills one round of
+    workgroups, so it runs one workgroup per (layer, KV head, query tile)
+    (the row-LSE-only attention kernel, not stream mode); W, smoothed keys
+    and kept sets against the oracle."""
     L = 28
     classes = [S] * 3 + [M] * 17 + [D] * 8
     wl = _wl("ext_guide_all", 55, L, 28, 4, 128, 256, 64, tuple(200 + 3 * l for l in range(L)))
