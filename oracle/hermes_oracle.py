@@ -46,9 +46,10 @@ Readings where the paper is silent or ambiguous (each is a parameter here):
   * attention scale 1/sqrt(d); row r sees the whole cache plus chunk rows
     0..r.
 
-Parity pins live in tests/test_oracle_pins.py.  The conventions listed above
-are "parity unpinned" against the paper (it prints no scores or kept sets);
-they are pinned only through closed forms, invariants and brute force.
+Parity pins live in tests/test_oracle_pins.py.  The paper prints no worked
+example with scores or kept sets, so no expected value here comes from it;
+every function and each reading above is pinned through closed forms,
+invariants, library routines (torch SDPA and softmax) and brute force.
 """
 from __future__ import annotations
 
