@@ -34,6 +34,9 @@ constexpr int BQS = 32;                  // packed rows per sweep tile
 constexpr int KPAD = 8;                  // u16 padding of K / Q rows in LDS
 constexpr int VPAD = 32;                 // u16 padding of V rows in LDS
 constexpr int kAheadK = 4;               // K fragment reads issued ahead of their MFMA
+// fourth word of a raw buffer descriptor on gfx9-family chips (32-bit data,
+// no swizzle; the range check uses the byte count in the third word)
+constexpr int kBufferWord3 = 0x00020000;
 constexpr int kAheadV = 4;               // V^T fragment pairs issued ahead of their MFMA
 
 __device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
@@ -180,13 +183,20 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
   __shared__ __attribute__((aligned(16))) uint16_t Ks[2][BN][D + KPAD];
   __shared__ __attribute__((aligned(16))) uint16_t Vs[2][BN][D + VPAD];
   uint4 kreg[NLD], vreg[NLD];
+  // pure tiles load through buffer descriptors whose base is the tile's first
+  // row (scalar arithmetic): each load is the descriptor plus the lane's
+  // 32-bit offset, with no per-lane 64-bit address addition
   auto load_pure = [&](int k0) {
-    const char *kb = reinterpret_cast<const char *>(kc + (int64_t)k0 * row_stride);
-    const char *vb = reinterpret_cast<const char *>(vc + (int64_t)k0 * row_stride);
+    const __amdgpu_buffer_rsrc_t kr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(kc + (int64_t)k0 * row_stride), 0, 0x7FFFFFFF, kBufferWord3);
+    const __amdgpu_buffer_rsrc_t vr = __builtin_amdgcn_make_buffer_rsrc(
+        (void *)(vc + (int64_t)k0 * row_stride), 0, 0x7FFFFFFF, kBufferWord3);
 #pragma unroll
     for (int uu = 0; uu < NLD; ++uu) {
-      kreg[uu] = gload16(reinterpret_cast<const uint16_t *>(kb + cofs[uu]));
-      vreg[uu] = gload16(reinterpret_cast<const uint16_t *>(vb + cofs[uu]));
+      const auto kx = __builtin_amdgcn_raw_buffer_load_b128(kr, (int)cofs[uu], 0, 0);
+      const auto vx = __builtin_amdgcn_raw_buffer_load_b128(vr, (int)cofs[uu], 0, 0);
+      kreg[uu] = uint4{kx[0], kx[1], kx[2], kx[3]};
+      vreg[uu] = uint4{vx[0], vx[1], vx[2], vx[3]};
     }
   };
   // a tile of any pair (its cache, new rows, lengths and KV head given)
@@ -222,7 +232,8 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
   float m_run = -1e30f, l_run = 0.f;
-  const float c = a.scale_log2;
+  const float c = a.scale_log2, inv_c = 1.f / c;
+  float m_lim = (m_run + 8.f) * inv_c;
 
   // transposed-read coordinates of this lane inside its 16-lane group
   const int g16 = lane >> 4, s16 = lane & 15;
@@ -275,14 +286,23 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
 #pragma unroll
       for (int jj = 0; jj < 16; ++jj) mx = fmaxf(mx, s[sub][jj]);
     }
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mt = mx * c;
+    {
+      // the other lane half's maximum (rows are split over the halves by key):
+      // v_permlane32_swap exchanges the halves of a register pair, so the max
+      // of its two results holds both halves' maxima in every lane
+      const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      const float m0 = __uint_as_float(r[0]), m1 = __uint_as_float(r[1]);
+      mx = m0 > m1 ? m0 : m1;   // (a compare and a select: fmaxf would first canonicalise both)
+    }
     // Lazy rescaling: the running maximum only moves when a row's tile
-    // maximum exceeds it by more than 2^8, so probabilities stay <= 256.
-    if (__any(mt > m_run + 8.f)) {
-      const float m_new = fmaxf(m_run, mt);
+    // maximum exceeds it by more than 2^8 (in the log2 domain), so
+    // probabilities stay <= 256; the test compares the raw maximum with the
+    // precomputed threshold (m_run + 8) / c.
+    if (__any(mx > m_lim)) {
+      const float m_new = fmaxf(m_run, mx * c);
       const float alpha = fast_exp2(m_run - m_new);
       m_run = m_new;
+      m_lim = (m_run + 8.f) * inv_c;
       l_run *= alpha;
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) o[db] *= alpha;
@@ -381,6 +401,7 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) o[db] = f32x16{};
         m_run = -1e30f;
+        m_lim = (m_run + 8.f) * inv_c;
         l_run = 0.f;
         t = 0;
         if (n_pure > 0) load_pure(0); else load_any(0);
@@ -396,6 +417,18 @@ __global__ __launch_bounds__(AT, 1) void attn_fwd(AttnArgs a, int nqt) {
     // body); the last pure tile joins the general loop, where it is unmasked.
     if (n_pure > 0) load_pure(0); else load_any(0);
     int t = 0;
+    // two tiles per trip, so that the LDS buffer of each is a constant and
+    // its addresses fold into the instructions' offsets
+    for (; t + 2 < n_pure; t += 2) {
+      store_tile(0);
+      __syncthreads();
+      load_pure((t + 1) * BN);
+      if (wave_rows) compute(0, t, NoMask{});
+      store_tile(1);
+      __syncthreads();
+      load_pure((t + 2) * BN);
+      if (wave_rows) compute(1, t + 1, NoMask{});
+    }
     for (; t + 1 < n_pure; ++t) {
       store_tile(t & 1);
       __syncthreads();
