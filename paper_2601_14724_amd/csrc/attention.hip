@@ -577,31 +577,36 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   auto tile_p = [&](int it) { return p_begin + it * BQS; };
   // Tiles are loaded in order, so each thread's packed row p = (r, g) steps
   // by BQS per tile: r by BQS / G and g by BQS % G, plus one row when g wraps
-  // past G; its address moves by the matching fixed amounts.
-  int ld_p[NLD], ld_g[NLD];
-  const uint16_t *ld_q[NLD];
+  // past G; its byte offset moves by the matching fixed amounts.  The loads
+  // go through a buffer descriptor over this slot's C chunk rows, so an
+  // offset is a 32-bit register and rows past P (r >= C) lie outside the
+  // descriptor's range, where the load returns zeros.
+  const __amdgpu_buffer_rsrc_t qrs =
+      __builtin_amdgcn_make_buffer_rsrc((void *)q, 0, C * Hq * D * (int)sizeof(uint16_t), kBufferWord3);
+  int ld_g[NLD];
+  uint32_t ld_o[NLD];
   const int step_r = BQS / G, step_g = BQS - (BQS / G) * G;
-  const int64_t dstep = (int64_t)(step_r * Hq + step_g) * D, dwrap = (int64_t)(Hq - G) * D;
+  const uint32_t ostep = (uint32_t)((step_r * Hq + step_g) * D * sizeof(uint16_t));
+  const uint32_t owrap = (uint32_t)((Hq - G) * D * sizeof(uint16_t));
 #pragma unroll
   for (int u = 0; u < NLD; ++u) {
-    ld_p[u] = p_begin + (tid + u * 256) / CH;
-    const int r0 = ld_p[u] / G;
-    ld_g[u] = ld_p[u] - r0 * G;
-    ld_q[u] = q + ((int64_t)r0 * Hq + kv_blk * G + ld_g[u]) * D + ((tid + u * 256) % CH) * 8;
+    const int p = p_begin + (tid + u * 256) / CH;
+    const int r0 = p / G;
+    ld_g[u] = p - r0 * G;
+    ld_o[u] = (uint32_t)((((int64_t)r0 * Hq + kv_blk * G + ld_g[u]) * D + ((tid + u * 256) % CH) * 8) *
+                         sizeof(uint16_t));
   }
-  // FULL: every row of the tile is < P (no bounds test on the loads)
+  // FULL: every row of the tile is < P (no bounds test on the LSE load)
   auto load_tile = [&](int it, auto full) {
     const int pt = tile_p(it);
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      uint4 v = {0u, 0u, 0u, 0u};
-      if (decltype(full)::value || ld_p[u] < P) v = gload16(ld_q[u]);
-      qreg[u] = v;
-      ld_p[u] += BQS;
+      const auto x = __builtin_amdgcn_raw_buffer_load_b128(qrs, (int)ld_o[u], 0, 0);
+      qreg[u] = uint4{x[0], x[1], x[2], x[3]};
       ld_g[u] += step_g;
       const bool wrap = ld_g[u] >= G;
       ld_g[u] -= wrap ? G : 0;
-      ld_q[u] += dstep + (wrap ? dwrap : 0);
+      ld_o[u] += ostep + (wrap ? owrap : 0u);
     }
     if (tid < BQS)
       lreg = (decltype(full)::value || pt + tid < P) ? lse_l[(int64_t)kv_blk * P + pt + tid] : INFINITY;
