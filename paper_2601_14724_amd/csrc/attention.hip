@@ -575,48 +575,48 @@ __global__ __launch_bounds__(256, 3) void attn_colsum(ColsumArgs a, int nkb) {
   uint4 qreg[NLD];
   float lreg = INFINITY;
   auto tile_p = [&](int it) { return p_begin + it * BQS; };
-  // Tiles are loaded in order, so each thread's packed row p = (r, g) steps
+  // Each thread loads NLD 16-byte pieces of one packed row of a tile (pieces
+  // c and c + CH / NLD, ...), so one offset per thread serves all of them.
+  // Tiles are loaded in order, so the thread's packed row p = (r, g) steps
   // by BQS per tile: r by BQS / G and g by BQS % G, plus one row when g wraps
   // past G; its byte offset moves by the matching fixed amounts.  The loads
-  // go through a buffer descriptor over this slot's C chunk rows, so an
+  // go through a buffer descriptor over this slot's C chunk rows, so the
   // offset is a 32-bit register and rows past P (r >= C) lie outside the
   // descriptor's range, where the load returns zeros.
+  constexpr int PPR = CH / NLD;             // pieces per thread-row group
+  const int ld_row = tid / PPR, ld_c = tid % PPR;
   const __amdgpu_buffer_rsrc_t qrs =
       __builtin_amdgcn_make_buffer_rsrc((void *)q, 0, C * Hq * D * (int)sizeof(uint16_t), kBufferWord3);
-  int ld_g[NLD];
-  uint32_t ld_o[NLD];
   const int step_r = BQS / G, step_g = BQS - (BQS / G) * G;
   const uint32_t ostep = (uint32_t)((step_r * Hq + step_g) * D * sizeof(uint16_t));
   const uint32_t owrap = (uint32_t)((Hq - G) * D * sizeof(uint16_t));
-#pragma unroll
-  for (int u = 0; u < NLD; ++u) {
-    const int p = p_begin + (tid + u * 256) / CH;
+  int ld_g;
+  uint32_t ld_o;
+  {
+    const int p = p_begin + ld_row;
     const int r0 = p / G;
-    ld_g[u] = p - r0 * G;
-    ld_o[u] = (uint32_t)((((int64_t)r0 * Hq + kv_blk * G + ld_g[u]) * D + ((tid + u * 256) % CH) * 8) *
-                         sizeof(uint16_t));
+    ld_g = p - r0 * G;
+    ld_o = (uint32_t)((((int64_t)r0 * Hq + kv_blk * G + ld_g) * D + ld_c * 8) * sizeof(uint16_t));
   }
   // FULL: every row of the tile is < P (no bounds test on the LSE load)
   auto load_tile = [&](int it, auto full) {
     const int pt = tile_p(it);
 #pragma unroll
     for (int u = 0; u < NLD; ++u) {
-      const auto x = __builtin_amdgcn_raw_buffer_load_b128(qrs, (int)ld_o[u], 0, 0);
+      const auto x = __builtin_amdgcn_raw_buffer_load_b128(qrs, (int)(ld_o + u * PPR * 16), 0, 0);
       qreg[u] = uint4{x[0], x[1], x[2], x[3]};
-      ld_g[u] += step_g;
-      const bool wrap = ld_g[u] >= G;
-      ld_g[u] -= wrap ? G : 0;
-      ld_o[u] += ostep + (wrap ? owrap : 0u);
     }
+    ld_g += step_g;
+    const bool wrap = ld_g >= G;
+    ld_g -= wrap ? G : 0;
+    ld_o += ostep + (wrap ? owrap : 0u);
     if (tid < BQS)
       lreg = (decltype(full)::value || pt + tid < P) ? lse_l[(int64_t)kv_blk * P + pt + tid] : INFINITY;
   };
   auto store_tile = [&](int b) {
 #pragma unroll
-    for (int u = 0; u < NLD; ++u) {
-      const int e = tid + u * 256;
-      *reinterpret_cast<uint4 *>(&Qs[b][e / CH][(e % CH) * 8]) = qreg[u];
-    }
+    for (int u = 0; u < NLD; ++u)
+      *reinterpret_cast<uint4 *>(&Qs[b][ld_row][(ld_c + u * PPR) * 8]) = qreg[u];
     if (tid < BQS) Ls[b][tid] = lreg;
   };
 
