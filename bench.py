@@ -35,7 +35,7 @@ PEAK_HBM_GBS = 8000.0         # MI355X HBM3E
 # and WRITE_SIZE counter passes in profiles/traffic_c3_7b_28layer.md (fetch
 # scaled x2.000, write x1.000 by a 256 MiB copy).  Valid only for the kernel
 # source it was measured on: reported as null once attention.hip changes.
-ATTN_TRAFFIC = {"bytes": 1.2034e9, "source_sha256_16": "8a87f4a0ffbf276f",
+ATTN_TRAFFIC = {"bytes": 1.2163e9, "source_sha256_16": "daa91be90110cf74",
                 "workload": "c3_7b_28layer"}
 
 
