@@ -125,6 +125,38 @@ def test_query_after_compress_matches_oracle(anchors):
     kv.close()
 
 
+def test_max_layer_count_step_and_query():
+    """HERMES_MAX_LAYERS (64) layers in one context: every per-layer table and
+    launch-argument array at its limit.  Budgets ramp across the layers so
+    that some evict and the last ones keep everything; the append + compress
+    step of every layer against the oracle, then an 8-token query over the
+    64 compacted caches of different lengths."""
+    from paper_2601_14724_amd import hermes as H
+    from paper_2601_14724_amd import streaming
+    L = H.MAX_LAYERS
+    budgets = [60 + (200 * l) // (L - 1) for l in range(L)]   # 60 .. 260 against T = 224
+    wl = wk.custom("maxlayers", 125, L, 4, 2, 64, 200, 24, budgets, query_len=8, anchor_period=29)
+    say(f"[maxlayers] {L} layers, budgets {budgets[0]}..{budgets[-1]}, T = 224")
+    caches, chunks = gen(wl)
+    kv, out, w = run_gpu_step(wl, caches, chunks, force_scores=True)
+    ref = orc.stream_step(oracle_caches(caches), oracle_chunks(chunks), oracle_config(wl))
+    bits = raw_bits(caches, chunks)
+    for l in range(L):
+        check_layer(l, kv, out, w, ref, wl.budgets[l], wl.chunk, report=bits)
+    assert [kv.length(l) for l in range(L)] == [min(224, b) for b in budgets]
+    qry = [wk.gen_query(wl, l) for l in range(L)]
+    qt = {k: streaming.bf16_tensor(np.stack([x[k] for x in qry]), "cuda") for k in ("q", "k", "v")}
+    o = kv.query(qt["q"], qt["k"], qt["v"]).float().cpu().numpy()
+    f64 = wk.bf16_bits_to_f64
+    for l in range(L):
+        k_g, v_g, p_g = kv.view(l)
+        cache = orc.LayerCache(k_g.float().double().cpu().numpy(), v_g.float().double().cpu().numpy(),
+                               p_g.cpu().numpy())
+        want = orc.query_attention(cache, f64(qry[l]["q"]), f64(qry[l]["k"]), f64(qry[l]["v"]))
+        check_o(o[l], want, f"[maxlayers] query layer {l} ({kv.length(l)} cached)")
+    kv.close()
+
+
 def test_determinism_bitwise():
     wl = wk.WORKLOADS["c1_0p5b_1layer"]
     caches, chunks = gen(wl)
