@@ -177,6 +177,14 @@ def test_degenerate_budgets_keep_one_evict_one_keep_all():
     _step_parity(wl, classes=[orc.MIDDLE, orc.DEEP, orc.DEEP])
 
 
+def test_first_chunk_larger_than_the_budget():
+    """An empty cache and a 150-token first chunk against budgets 40, 75 and
+    149: every layer evicts among the chunk's own tokens, whose candidates
+    are each seen by a different number of chunk rows (Eq.2 with T0 = 0)."""
+    wl = wk.custom("first_chunk_evicts", 126, 3, 8, 2, 64, 0, 150, [40, 75, 149])
+    _step_parity(wl)
+
+
 def test_long_layers_past_the_lds_staging_limits():
     """40000 cached + 32 new candidates: the selection keys no longer fit in
     LDS (read from global memory), the partner positions of the layer above
