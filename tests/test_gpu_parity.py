@@ -194,8 +194,8 @@ def test_long_layers_past_the_lds_staging_limits():
     _step_parity(wl, classes=[orc.MIDDLE, orc.DEEP])
 
 
-@pytest.mark.parametrize("anchors", [0, 61])
-def test_query_stream_mode_over_unequal_caches(anchors):
+@pytest.mark.parametrize("anchors,n_q", [(0, 9), (61, 9), (61, 1)])
+def test_query_stream_mode_over_unequal_caches(anchors, n_q):
     """Layers of very different cache lengths (300, 2000 and 8000 tokens): the
     host runs the query in stream mode, the 326 key tiles of the six (layer,
     KV head) pairs cut into 256 unit ranges, so the longest layer's keys are
@@ -205,7 +205,7 @@ def test_query_stream_mode_over_unequal_caches(anchors):
     a block merged with a wrong weight, or dropped, moves the output by far
     more than the bars."""
     from paper_2601_14724_amd import streaming
-    wl = wk.custom("slices", 123, 3, 4, 2, 64, 8000, 9, (8000, 8000, 8000), query_len=9,
+    wl = wk.custom("slices", 123, 3, 4, 2, 64, 8000, 9, (8000, 8000, 8000), query_len=n_q,
                    anchor_period=anchors)
     lens = (300, 2000, 8000)
     caches = []
@@ -222,7 +222,7 @@ def test_query_stream_mode_over_unequal_caches(anchors):
         cache = orc.LayerCache(f64(caches[l]["k"]), f64(caches[l]["v"]),
                                caches[l]["pos"].astype(np.int64))
         want = orc.query_attention(cache, f64(qry[l]["q"]), f64(qry[l]["k"]), f64(qry[l]["v"]))
-        check_o(o[l], want, f"[stream] layer {l} ({lens[l]} cached, anchors {anchors})")
+        check_o(o[l], want, f"[stream] layer {l} ({lens[l]} cached, anchors {anchors}, {n_q} tokens)")
     kv.close()
 
 
